@@ -1,0 +1,196 @@
+#!/usr/bin/env python3
+"""Benchmark: cross-mesh resharding throughput on one MI355X.
+
+One step = one reshard_execute of the whole resharding task (one fused
+kernel launch reading every unique slice once and writing every destination
+shard, replicas included) over inputs already resident in HBM.  The plan
+(decomposition, sender choice, lowering) is built once before the timed
+region, as a resharding task is planned once and repeated every iteration.
+Its cost is reported separately as plan_us.
+
+Prints ONE JSON line.  Default workload: fp16 [8,2048,12288] (403 MB), source
+mesh (4,8) "R R S^{01}" -> destination mesh (4,8) "R S^1 R" (4x replicated),
+i.e. 384 MiB read + 1536 MiB written per step.
+"""
+
+from __future__ import annotations
+
+import argparse
+import hashlib
+import json
+import os
+import statistics
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+HBM_PEAK_GBS = 8000.0  # MI355X HBM3E, 8 TB/s
+METRIC = "effective resharding GB/s (read+write) and % of MI355X HBM peak, 1 GPU"
+TRAFFIC_FILE = os.path.join(ROOT, "profiles", "traffic_counters.json")
+KERNEL_SOURCES = [os.path.join(ROOT, "paper_2211_05322_amd", "csrc", f) for f in ("execute.hip", "desc.h", "planner.cpp")]
+
+
+def kernel_hash():
+    h = hashlib.sha256()
+    for f in KERNEL_SOURCES:
+        with open(f, "rb") as fh:
+            h.update(fh.read())
+    return h.hexdigest()[:16]
+
+
+def measured_traffic(workload_name):
+    """HBM bytes per launch from committed rocprofv3 counter runs, if they match this kernel."""
+    try:
+        with open(TRAFFIC_FILE) as f:
+            rec = json.load(f).get(workload_name)
+    except (OSError, ValueError):
+        return None
+    if not rec or rec.get("kernel_hash") != kernel_hash():
+        return None
+    return rec.get("hbm_bytes_per_launch")
+
+
+def cpu_baseline(w, src_dev, budget_s):
+    """The numpy oracle on host cores, on the same workload (bounded repeat count)."""
+    import numpy as np
+
+    import oracle
+    from paper_2211_05322_amd.workloads import as_numpy_bits
+
+    src = [as_numpy_bits(t) for t in src_dev]
+    es = src[0].dtype.itemsize
+    rd, wr = oracle.traffic_bytes(w.shape, es, w.dst_mesh, w.dst_spec)
+    times = []
+    t_start = time.perf_counter()
+    while True:
+        t0 = time.perf_counter()
+        out = oracle.reshard(src, w.shape, w.src_mesh, w.src_spec, w.dst_mesh, w.dst_spec)
+        times.append(time.perf_counter() - t0)
+        del out
+        if time.perf_counter() - t_start >= budget_s or len(times) >= 5:
+            break
+    med = statistics.median(times)
+    ncores = len(os.sched_getaffinity(0))
+    return {"value": round((rd + wr) / med / 1e9, 3), "unit": "GB/s", "cores": 1, "kind": "oracle",
+            "sample": f"full workload, {len(times)} run(s) of unshard+reshard in numpy on raw bits, "
+                      f"median {med:.3f} s; 1 thread used of {ncores} host cores; "
+                      f"bytes counted as read {rd} + written {wr}"}
+
+
+def main():
+    ap = argparse.ArgumentParser(description=__doc__.splitlines()[0])
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=50)
+    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--config", type=int, default=None, help="workload id 1..5 (default 5)")
+    ap.add_argument("--seed", type=int, default=0)
+    ap.add_argument("--chunk-bytes", type=int, default=0)
+    ap.add_argument("--block-threads", type=int, default=0)
+    ap.add_argument("--flags", type=int, default=0)
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--cpu-budget", type=float, default=10.0, help="seconds of oracle timing")
+    args = ap.parse_args()
+
+    if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
+        print("bench.py measures one GPU only: every mesh device is a buffer on a single MI355X; "
+              "multi-GPU resharding is not part of this build (use --gpus 1)", file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+
+    from paper_2211_05322_amd import binding as B
+    from paper_2211_05322_amd.workloads import BENCH_WORKLOAD, WORKLOADS, make_workload_tensor
+
+    wid = args.config or BENCH_WORKLOAD
+    w = WORKLOADS[wid]
+    if not torch.cuda.is_available():
+        print("no GPU visible", file=sys.stderr)
+        sys.exit(1)
+    B.load()
+    dev = torch.device("cuda", 0)
+    torch.cuda.set_device(dev)
+    stream = torch.cuda.current_stream()
+
+    # Inputs: the logical tensor is generated on the GPU and laid out on the
+    # source mesh by the library itself (a reshard from one buffer).
+    x = make_workload_tensor(w, seed=args.seed, device="cuda")
+    rep = "".join("R" for _ in w.shape)
+    scatter = B.reshard_plan(w.shape, w.dtype, (1,), rep, w.src_mesh, w.src_spec)
+    src = B.empty_shards(scatter, 1)
+    B.reshard_execute(scatter, [x], src)
+
+    t0 = time.perf_counter()
+    plan = B.reshard_plan(w.shape, w.dtype, w.src_mesh, w.src_spec, w.dst_mesh, w.dst_spec,
+                          flags=args.flags, chunk_bytes=args.chunk_bytes, block_threads=args.block_threads)
+    plan_us = (time.perf_counter() - t0) * 1e6
+    st = B.reshard_plan_stats(plan)
+    dst = B.empty_shards(plan, 1)
+    torch.cuda.synchronize()
+
+    for _ in range(args.warmup):
+        B.reshard_execute(plan, src, dst, stream=stream)
+    torch.cuda.synchronize()
+
+    ev0 = torch.cuda.Event(enable_timing=True)
+    ev1 = torch.cuda.Event(enable_timing=True)
+    h0 = time.perf_counter()
+    ev0.record(stream)
+    for _ in range(args.steps):
+        B.reshard_execute(plan, src, dst, stream=stream)
+    ev1.record(stream)
+    host_us = (time.perf_counter() - h0) * 1e6 / args.steps
+    torch.cuda.synchronize()
+    ms_total = ev0.elapsed_time(ev1)
+    ms_per_step = ms_total / args.steps
+
+    # Round-trip check through the library: dst -> one buffer must equal x.
+    back_plan = B.reshard_plan(w.shape, w.dtype, w.dst_mesh, w.dst_spec, (1,), rep)
+    back = B.empty_shards(back_plan, 1)
+    B.reshard_execute(back_plan, dst, back)
+    torch.cuda.synchronize()
+    roundtrip_ok = bool(torch.equal(back[0].view(torch.uint8), x.view(torch.uint8)))
+    del back
+
+    nbytes = st["bytes_read"] + st["bytes_written"]
+    gbs = nbytes / (ms_per_step * 1e-3) / 1e9
+    traffic = measured_traffic(w.name)
+    out = {
+        "metric": METRIC,
+        "value": round(gbs, 2),
+        "unit": "GB/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms_per_step, 5),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": {1: "u8", 2: "f16", 4: "f32", 8: "f64"}[x.element_size()] if w.dtype != "bfloat16" else "bf16",
+        "data": "synthetic",
+        "config": {
+            "workload": w.name, "shape": list(w.shape), "src_mesh": list(w.src_mesh), "src_spec": w.src_spec,
+            "dst_mesh": list(w.dst_mesh), "dst_spec": w.dst_spec, "bytes_read": st["bytes_read"],
+            "bytes_written": st["bytes_written"], "unit_tasks": st["n_unit_tasks"],
+            "workgroups": st["n_descriptors"], "max_fanout": st["max_fanout"],
+        },
+        "pct_of_hbm_peak": round(100.0 * gbs / HBM_PEAK_GBS, 2),
+        "roofline": {
+            "bound": "hbm", "achieved": round(gbs, 2), "peak": HBM_PEAK_GBS, "unit": "GB/s",
+            "frac": round(gbs / HBM_PEAK_GBS, 4), "traffic": traffic,
+        },
+        "plan_us": round(plan_us, 1),
+        "host_us_per_execute": round(host_us, 2),
+        "roundtrip_ok": roundtrip_ok,
+        "kernel_hash": kernel_hash(),
+    }
+    if not args.no_cpu_baseline:
+        out["cpu_baseline"] = cpu_baseline(w, src, args.cpu_budget)
+    print(json.dumps(out), flush=True)
+    if not roundtrip_ok:
+        sys.exit(3)
+
+
+if __name__ == "__main__":
+    main()

@@ -1,0 +1,198 @@
+/*
+ * reshard.h -- C ABI of libreshard.so: cross-mesh resharding on one MI355X.
+ *
+ * Problem (Zhuang et al., "On Optimizing the Communication of Model
+ * Parallelism", MLSys 2023, Section 2.2 "Cross-mesh resharding"): a tensor D
+ * laid out on a source device mesh under sharding spec X_A must be laid out
+ * on a disjoint destination mesh under spec X_B.  The library decomposes the
+ * task into unit communication tasks (one per unique data slice, Section 2.2
+ * and the appendix decomposition), picks one sender per slice among the
+ * source replicas (Section 3.2), and moves every slice with one fused HIP
+ * kernel that reads it once and writes it to every receiver (the broadcast
+ * strategy of Section 3.1: one sender, all receivers).
+ *
+ * On one GPU every mesh "device" is a separate buffer in the GPU's memory.
+ *
+ * Conventions shared by all calls
+ * -------------------------------
+ *  - Meshes are n-dimensional (1..8 axes).  Devices are numbered row-major
+ *    over mesh coordinates: the (2,2) mesh is [[0,1],[2,3]] (Section 2.2,
+ *    "Device mesh").  Pointer arrays are indexed by that number.
+ *  - A spec has one letter per tensor dimension (Section 2.2, "Sharding
+ *    spec"): "R" (replicated) or "S" followed by the mesh axes the dimension
+ *    is split over, major to minor, e.g. "S^0RR", "RS^{01}R", "S_{0}RR",
+ *    "S0 R S1".  Spaces and commas between letters are ignored.  A mesh axis
+ *    may appear at most once; axes no dimension uses replicate.
+ *  - For axes (a1,...,ap) a device at coordinates c holds shard number
+ *    j = c[a1]*m[a2]*...*m[ap] + ... + c[ap] of the m[a1]*...*m[ap] shards.
+ *  - A dimension of length l split into k shards gives shard j the range
+ *    [j*floor(l/k) + min(j, l mod k), +floor(l/k) + (j < l mod k)): the first
+ *    l mod k shards are one longer (66 into 4 is 17,17,16,16).  No padding.
+ *  - Each device buffer is the dense C-order (row-major) array of its shard;
+ *    its shape is given by reshard_plan_local_shape.  Shards of zero size are
+ *    allowed and their pointer may be NULL.
+ *  - Elements are opaque: only the byte size of the dtype matters, and bits
+ *    are copied exactly (NaN payloads, -0 and infinities included).
+ *  - Every call returns a status and never throws or aborts.  On failure
+ *    reshard_last_error() describes the reason.
+ */
+#ifndef RESHARD_H
+#define RESHARD_H
+
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef struct reshard_plan_s reshard_plan_t;  /* opaque; created by reshard_plan */
+
+typedef enum {
+    RESHARD_OK = 0,
+    RESHARD_EINVAL = 1,       /* bad argument: spec, mesh, shape, pointer, alignment */
+    RESHARD_EUNSUPPORTED = 2, /* valid but beyond a compiled limit (see below) */
+    RESHARD_ENOMEM = 3,       /* host or device allocation failed */
+    RESHARD_EHIP = 4          /* a HIP runtime call or kernel launch failed */
+} reshard_status_t;
+
+/* Element types.  Only the byte size (1, 2, 4 or 8) is used. */
+typedef enum {
+    RESHARD_U8 = 0, RESHARD_I8 = 1, RESHARD_F16 = 2, RESHARD_BF16 = 3,
+    RESHARD_F32 = 4, RESHARD_I32 = 5, RESHARD_F64 = 6, RESHARD_I64 = 7,
+    RESHARD_U16 = 8, RESHARD_I16 = 9, RESHARD_U32 = 10, RESHARD_U64 = 11
+} reshard_dtype_t;
+
+/* reshard_plan flags */
+#define RESHARD_SENDER_NAIVE 0x1u  /* lowest-indexed owner sends (Section 3.2, "Naive
+                                      algorithm"); default is longest-first greedy
+                                      balancing of sent bytes per device (Eq. 4). */
+#define RESHARD_NO_XCD_REMAP 0x2u  /* launch chunks in table order instead of giving each
+                                      XCD a contiguous run of chunks. */
+
+/* Compiled limits (RESHARD_EUNSUPPORTED beyond them). */
+#define RESHARD_MAX_NDIM 8
+#define RESHARD_MAX_MESH_NDIM 8
+#define RESHARD_MAX_BUFFERS 496    /* source + destination devices of one plan */
+
+/* Optional tuning of the lowering; zero fields take the defaults. */
+typedef struct {
+    int64_t chunk_bytes;    /* source bytes per workgroup chunk (default: sized to fill
+                               256 CUs, 4 KiB..256 KiB); rounded to whole vectors */
+    int32_t block_threads;  /* threads per workgroup: 64, 128, 256, 512 or 1024 (default 256) */
+    int32_t reserved[5];    /* must be zero */
+} reshard_tuning_t;
+
+/*
+ * Build a plan for resharding a tensor of shape[ndim] (ndim 1..8, each
+ * shape[i] >= 0) with elements of `dtype` from src_mesh (src_mesh_ndim axes,
+ * each >= 1) under src_spec to dst_mesh under dst_spec.
+ *
+ * Host only, thread-safe, no HIP call.  Computes per-device shard boxes, the
+ * unit tasks (non-empty intersections of source and destination shards, each
+ * with its owners and its receivers; Section 2.2 and the appendix), the
+ * sender of each (flags), and the descriptor table the kernel runs from.
+ * The source and destination meshes are disjoint sets of buffers (Section 2.2).
+ *
+ * On success *out owns a new plan (free with reshard_plan_destroy).
+ * Errors: EINVAL for a malformed spec, spec length != ndim, an axis outside the
+ * mesh or used twice, ndim or mesh_ndim outside 1..8, a negative dimension, a
+ * mesh axis < 1, NULL shape/mesh/spec/out; EUNSUPPORTED when the two meshes
+ * together have more than RESHARD_MAX_BUFFERS devices; ENOMEM on allocation
+ * failure.  *out is set to NULL on error.
+ */
+reshard_status_t reshard_plan(int ndim, const int64_t *shape, reshard_dtype_t dtype,
+                              int src_mesh_ndim, const int64_t *src_mesh, const char *src_spec,
+                              int dst_mesh_ndim, const int64_t *dst_mesh, const char *dst_spec,
+                              unsigned flags, reshard_plan_t **out);
+
+/* As reshard_plan, with lowering knobs (NULL = defaults).  EINVAL for a bad
+ * block size, a negative chunk size or non-zero reserved fields. */
+reshard_status_t reshard_plan_ex(int ndim, const int64_t *shape, reshard_dtype_t dtype,
+                                 int src_mesh_ndim, const int64_t *src_mesh, const char *src_spec,
+                                 int dst_mesh_ndim, const int64_t *dst_mesh, const char *dst_spec,
+                                 unsigned flags, const reshard_tuning_t *tuning,
+                                 reshard_plan_t **out);
+
+/*
+ * Run the plan: fill every destination buffer from the source buffers.
+ *
+ * src_ptrs[k] (k < number of source devices) and dst_ptrs[k] (k < number of
+ * destination devices) are device pointers on the current HIP device, each to
+ * the dense C-order shard of that device, owned by the caller.  A pointer may
+ * be NULL only if its shard is empty.  Pointers must be aligned to
+ * reshard_plan_alignment() bytes.  Source and destination buffers must not
+ * overlap.  `stream` is a hipStream_t (NULL = the null stream).
+ *
+ * Asynchronous and stream-ordered: it enqueues one kernel and returns.  The
+ * first call on a device uploads the descriptor table to memory the plan owns
+ * (one hipMalloc + synchronous copy); later calls only launch.  A plan may be
+ * executed any number of times, on any stream; calls on different streams
+ * that write the same destination buffers race, as any two kernels would.
+ *
+ * Errors: EINVAL for NULL plan or pointer arrays, a NULL or misaligned buffer
+ * for a non-empty shard; ENOMEM if the table upload cannot allocate; EHIP if a
+ * HIP call or the launch fails.
+ */
+reshard_status_t reshard_execute(const reshard_plan_t *plan, void *const *src_ptrs,
+                                 void *const *dst_ptrs, void *stream);
+
+/* Free a plan and its device table.  NULL is accepted.  The caller must make
+ * sure no launched execute of this plan is still running. */
+void reshard_plan_destroy(reshard_plan_t *plan);
+
+/* Shape of device `device`'s shard on side 0 (source) or 1 (destination):
+ * writes ndim values to shape_out.  EINVAL for a bad side/device/NULL. */
+reshard_status_t reshard_plan_local_shape(const reshard_plan_t *plan, int side, int64_t device,
+                                          int64_t *shape_out);
+
+/* Plan totals (any output pointer may be NULL):
+ *  bytes_read    = bytes of D, each unique slice read once (the lower bound of
+ *                  Section 2.2);
+ *  bytes_written = sum of all destination shard sizes (replicas counted);
+ *  n_unit_tasks, n_descriptors (workgroup chunks), max_fanout (largest
+ *  receiver count of a unit task). */
+reshard_status_t reshard_plan_stats(const reshard_plan_t *plan, int64_t *bytes_read,
+                                    int64_t *bytes_written, int64_t *n_unit_tasks,
+                                    int64_t *n_descriptors, int64_t *max_fanout);
+
+/* Required byte alignment of every buffer pointer passed to reshard_execute
+ * (1..16), or 0 for a NULL plan. */
+int64_t reshard_plan_alignment(const reshard_plan_t *plan);
+
+/*
+ * Unit task `index` (0 <= index < n_unit_tasks), in lexicographic order of the
+ * slice's lower corner.  Writes lo[ndim] and hi[ndim] (the slice is
+ * [lo, hi) per dimension of D), the chosen sender, all owners (senders,
+ * ascending, up to senders_cap written, total in *n_senders) and all
+ * receivers (ascending, up to receivers_cap written, total in *n_receivers).
+ * Output pointers may be NULL when their capacity is 0.  EINVAL for a bad
+ * index or NULL plan/lo/hi.
+ */
+reshard_status_t reshard_plan_unit_task(const reshard_plan_t *plan, int64_t index,
+                                        int64_t *lo, int64_t *hi, int64_t *chosen_sender,
+                                        int64_t *senders, int64_t senders_cap, int64_t *n_senders,
+                                        int64_t *receivers, int64_t receivers_cap,
+                                        int64_t *n_receivers);
+
+/*
+ * Run the plan's descriptor table on HOST memory with a plain loop: the same
+ * table, index arithmetic and fan-out the kernel uses, so the lowering can be
+ * checked on a machine without a GPU.  Never called by reshard_execute.
+ * src_ptrs/dst_ptrs are host pointers with the layout described above.
+ * EINVAL for NULL arguments or a NULL buffer of a non-empty shard.
+ */
+reshard_status_t reshard_debug_execute_host(const reshard_plan_t *plan, void *const *src_ptrs,
+                                            void *const *dst_ptrs);
+
+/* Text of the last error on the calling thread ("" if none).  Never NULL;
+ * valid until the next call on the same thread. */
+const char *reshard_last_error(void);
+
+/* Library version string, e.g. "0.1.0". */
+const char *reshard_version(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* RESHARD_H */

@@ -1,0 +1,247 @@
+// capi.cpp -- C ABI of libreshard.so: planning, queries, host interpreter.
+// reshard_execute and the kernel live in execute.hip.
+#include <cstring>
+#include <new>
+#include <string>
+
+#include "../../include/reshard.h"
+#include "planner.hpp"
+
+namespace rs {
+// Defined in execute.hip: frees the plan's device table (if any).
+void release_device_table(const Plan &p);
+
+thread_local std::string g_last_error;
+
+reshard_status_t fail(reshard_status_t st, const std::string &msg) {
+    g_last_error = msg;
+    return st;
+}
+}  // namespace rs
+
+using rs::fail;
+
+namespace {
+
+int64_t elem_size(reshard_dtype_t dt) {
+    switch (dt) {
+        case RESHARD_U8: case RESHARD_I8: return 1;
+        case RESHARD_F16: case RESHARD_BF16: case RESHARD_U16: case RESHARD_I16: return 2;
+        case RESHARD_F32: case RESHARD_I32: case RESHARD_U32: return 4;
+        case RESHARD_F64: case RESHARD_I64: case RESHARD_U64: return 8;
+    }
+    return 0;
+}
+
+bool mul_ok(int64_t a, int64_t b, int64_t limit, int64_t &out) {
+    if (a != 0 && b > limit / a) return false;
+    out = a * b;
+    return true;
+}
+
+reshard_status_t check_mesh(const char *side, int mesh_ndim, const int64_t *mesh, int64_t &ndev) {
+    if (mesh_ndim < 1 || mesh_ndim > RESHARD_MAX_MESH_NDIM)
+        return fail(RESHARD_EINVAL, std::string(side) + " mesh must have 1..8 axes, got " + std::to_string(mesh_ndim));
+    if (!mesh) return fail(RESHARD_EINVAL, std::string(side) + " mesh pointer is NULL");
+    ndev = 1;
+    for (int i = 0; i < mesh_ndim; ++i) {
+        if (mesh[i] < 1)
+            return fail(RESHARD_EINVAL, std::string(side) + " mesh axis " + std::to_string(i) + " is " +
+                                            std::to_string(mesh[i]) + "; must be >= 1");
+        if (!mul_ok(ndev, mesh[i], RESHARD_MAX_BUFFERS, ndev))
+            return fail(RESHARD_EUNSUPPORTED, std::string(side) + " mesh has more than " +
+                                                  std::to_string(RESHARD_MAX_BUFFERS) + " devices");
+    }
+    return RESHARD_OK;
+}
+
+reshard_status_t make_plan(int ndim, const int64_t *shape, reshard_dtype_t dtype, int smn, const int64_t *sm,
+                           const char *sspec, int dmn, const int64_t *dm, const char *dspec, unsigned flags,
+                           const reshard_tuning_t *tuning, reshard_plan_t **out) {
+    if (!out) return fail(RESHARD_EINVAL, "out is NULL");
+    *out = nullptr;
+    if (ndim < 1 || ndim > RESHARD_MAX_NDIM)
+        return fail(RESHARD_EINVAL, "ndim must be 1..8, got " + std::to_string(ndim));
+    if (!shape) return fail(RESHARD_EINVAL, "shape is NULL");
+    const int64_t es = elem_size(dtype);
+    if (es == 0) return fail(RESHARD_EINVAL, "unknown dtype " + std::to_string(int(dtype)));
+    int64_t total = es;
+    for (int i = 0; i < ndim; ++i) {
+        if (shape[i] < 0) return fail(RESHARD_EINVAL, "shape[" + std::to_string(i) + "] is negative");
+        if (!mul_ok(total, shape[i], int64_t(1) << 56, total))
+            return fail(RESHARD_EUNSUPPORTED, "tensor larger than 2^56 bytes");
+    }
+    if (flags & ~(RESHARD_SENDER_NAIVE | RESHARD_NO_XCD_REMAP))
+        return fail(RESHARD_EINVAL, "unknown flag bits");
+    rs::Tuning tn;
+    if (tuning) {
+        for (int r : tuning->reserved)
+            if (r != 0) return fail(RESHARD_EINVAL, "tuning.reserved must be zero");
+        if (tuning->chunk_bytes < 0) return fail(RESHARD_EINVAL, "tuning.chunk_bytes is negative");
+        const int bt = tuning->block_threads;
+        if (bt != 0 && bt != 64 && bt != 128 && bt != 256 && bt != 512 && bt != 1024)
+            return fail(RESHARD_EINVAL, "tuning.block_threads must be 64, 128, 256, 512 or 1024");
+        tn.chunk_bytes = tuning->chunk_bytes;
+        if (bt) tn.block_threads = bt;
+    }
+    int64_t ns = 0, nd = 0;
+    reshard_status_t st = check_mesh("source", smn, sm, ns);
+    if (st != RESHARD_OK) return st;
+    st = check_mesh("destination", dmn, dm, nd);
+    if (st != RESHARD_OK) return st;
+    if (ns + nd > RESHARD_MAX_BUFFERS)
+        return fail(RESHARD_EUNSUPPORTED, "source and destination meshes have " + std::to_string(ns + nd) +
+                                              " devices; at most " + std::to_string(RESHARD_MAX_BUFFERS));
+    std::vector<std::vector<int>> sax, dax;
+    std::string err = rs::parse_spec(sspec, ndim, smn, sax);
+    if (!err.empty()) return fail(RESHARD_EINVAL, "source " + err);
+    err = rs::parse_spec(dspec, ndim, dmn, dax);
+    if (!err.empty()) return fail(RESHARD_EINVAL, "destination " + err);
+
+    rs::Plan *p = new (std::nothrow) rs::Plan();
+    if (!p) return fail(RESHARD_ENOMEM, "out of host memory");
+    try {
+        p->ndim = ndim;
+        p->shape.assign(shape, shape + ndim);
+        p->es = es;
+        p->flags = flags;
+        p->tuning = tn;
+        rs::build_layout(p->shape, std::vector<int64_t>(sm, sm + smn), sax, p->src);
+        rs::build_layout(p->shape, std::vector<int64_t>(dm, dm + dmn), dax, p->dst);
+        // bound the number of unit tasks before enumerating them
+        int64_t bound = 1;
+        for (int d = 0; d < ndim; ++d)
+            if (!mul_ok(bound, p->src.nshards[d] + p->dst.nshards[d], int64_t(1) << 24, bound)) {
+                delete p;
+                return fail(RESHARD_EUNSUPPORTED, "more than 2^24 unit tasks");
+            }
+        rs::build_tasks(*p);
+        rs::choose_senders(*p);
+        rs::lower(*p);
+        if (p->too_many) {
+            delete p;
+            return fail(RESHARD_EUNSUPPORTED, "lowering needs more than 2^24 workgroup chunks");
+        }
+    } catch (const std::bad_alloc &) {
+        delete p;
+        return fail(RESHARD_ENOMEM, "out of host memory while planning");
+    }
+    *out = reinterpret_cast<reshard_plan_t *>(p);
+    return RESHARD_OK;
+}
+
+const rs::Plan *as_plan(const reshard_plan_t *p) { return reinterpret_cast<const rs::Plan *>(p); }
+
+}  // namespace
+
+extern "C" {
+
+reshard_status_t reshard_plan(int ndim, const int64_t *shape, reshard_dtype_t dtype, int src_mesh_ndim,
+                              const int64_t *src_mesh, const char *src_spec, int dst_mesh_ndim,
+                              const int64_t *dst_mesh, const char *dst_spec, unsigned flags,
+                              reshard_plan_t **out) {
+    return make_plan(ndim, shape, dtype, src_mesh_ndim, src_mesh, src_spec, dst_mesh_ndim, dst_mesh, dst_spec,
+                     flags, nullptr, out);
+}
+
+reshard_status_t reshard_plan_ex(int ndim, const int64_t *shape, reshard_dtype_t dtype, int src_mesh_ndim,
+                                 const int64_t *src_mesh, const char *src_spec, int dst_mesh_ndim,
+                                 const int64_t *dst_mesh, const char *dst_spec, unsigned flags,
+                                 const reshard_tuning_t *tuning, reshard_plan_t **out) {
+    return make_plan(ndim, shape, dtype, src_mesh_ndim, src_mesh, src_spec, dst_mesh_ndim, dst_mesh, dst_spec,
+                     flags, tuning, out);
+}
+
+void reshard_plan_destroy(reshard_plan_t *plan) {
+    if (!plan) return;
+    rs::Plan *p = reinterpret_cast<rs::Plan *>(plan);
+    rs::release_device_table(*p);
+    delete p;
+}
+
+reshard_status_t reshard_plan_local_shape(const reshard_plan_t *plan, int side, int64_t device,
+                                          int64_t *shape_out) {
+    const rs::Plan *p = as_plan(plan);
+    if (!p || !shape_out) return fail(RESHARD_EINVAL, "NULL plan or shape_out");
+    if (side != 0 && side != 1) return fail(RESHARD_EINVAL, "side must be 0 (source) or 1 (destination)");
+    const int64_t n = side == 0 ? p->src.ndev : p->dst.ndev;
+    if (device < 0 || device >= n)
+        return fail(RESHARD_EINVAL, "device " + std::to_string(device) + " outside 0.." + std::to_string(n - 1));
+    rs::local_shape(*p, side, device, shape_out);
+    return RESHARD_OK;
+}
+
+reshard_status_t reshard_plan_stats(const reshard_plan_t *plan, int64_t *bytes_read, int64_t *bytes_written,
+                                    int64_t *n_unit_tasks, int64_t *n_descriptors, int64_t *max_fanout) {
+    const rs::Plan *p = as_plan(plan);
+    if (!p) return fail(RESHARD_EINVAL, "NULL plan");
+    if (bytes_read) *bytes_read = p->bytes_read;
+    if (bytes_written) *bytes_written = p->bytes_written;
+    if (n_unit_tasks) *n_unit_tasks = int64_t(p->tasks.size());
+    if (n_descriptors) *n_descriptors = int64_t(p->descs.size());
+    if (max_fanout) *max_fanout = p->max_fanout;
+    return RESHARD_OK;
+}
+
+int64_t reshard_plan_alignment(const reshard_plan_t *plan) {
+    const rs::Plan *p = as_plan(plan);
+    return p ? p->align : 0;
+}
+
+reshard_status_t reshard_plan_unit_task(const reshard_plan_t *plan, int64_t index, int64_t *lo, int64_t *hi,
+                                        int64_t *chosen_sender, int64_t *senders, int64_t senders_cap,
+                                        int64_t *n_senders, int64_t *receivers, int64_t receivers_cap,
+                                        int64_t *n_receivers) {
+    const rs::Plan *p = as_plan(plan);
+    if (!p || !lo || !hi) return fail(RESHARD_EINVAL, "NULL plan, lo or hi");
+    if (index < 0 || index >= int64_t(p->tasks.size()))
+        return fail(RESHARD_EINVAL, "unit task index " + std::to_string(index) + " out of range");
+    if ((senders_cap > 0 && !senders) || (receivers_cap > 0 && !receivers) || senders_cap < 0 || receivers_cap < 0)
+        return fail(RESHARD_EINVAL, "NULL output array with non-zero capacity");
+    const rs::UnitTask &t = p->tasks[size_t(index)];
+    for (int d = 0; d < p->ndim; ++d) {
+        lo[d] = t.lo[d];
+        hi[d] = t.hi[d];
+    }
+    if (chosen_sender) *chosen_sender = t.sender;
+    const int64_t s0 = p->src.shard_devs_off[t.src_shard], s1 = p->src.shard_devs_off[t.src_shard + 1];
+    for (int64_t k = s0; k < s1 && k - s0 < senders_cap; ++k) senders[k - s0] = p->src.shard_devs[k];
+    if (n_senders) *n_senders = s1 - s0;
+    const int64_t r0 = p->dst.shard_devs_off[t.dst_shard], r1 = p->dst.shard_devs_off[t.dst_shard + 1];
+    for (int64_t k = r0; k < r1 && k - r0 < receivers_cap; ++k) receivers[k - r0] = p->dst.shard_devs[k];
+    if (n_receivers) *n_receivers = r1 - r0;
+    return RESHARD_OK;
+}
+
+reshard_status_t reshard_debug_execute_host(const reshard_plan_t *plan, void *const *src_ptrs,
+                                            void *const *dst_ptrs) {
+    const rs::Plan *p = as_plan(plan);
+    if (!p || !src_ptrs || !dst_ptrs) return fail(RESHARD_EINVAL, "NULL plan or pointer array");
+    for (int64_t k = 0; k < p->src.ndev; ++k)
+        if (p->src_local_numel[k] > 0 && !src_ptrs[k])
+            return fail(RESHARD_EINVAL, "source buffer " + std::to_string(k) + " is NULL but its shard is not empty");
+    for (int64_t k = 0; k < p->dst.ndev; ++k)
+        if (p->dst_local_numel[k] > 0 && !dst_ptrs[k])
+            return fail(RESHARD_EINVAL, "destination buffer " + std::to_string(k) + " is NULL but its shard is not empty");
+    for (const rs::Desc &d : p->descs) {
+        const uint32_t w = 1u << rs::kind_log2w(d.kind);
+        const uint32_t levels = rs::kind_levels(d.kind);
+        const char *src = static_cast<const char *>(src_ptrs[d.src_buf]);
+        for (uint32_t v = d.v0; v < d.v1; ++v) {
+            const rs::Offsets o = levels == 1   ? rs::piece_offsets<1>(d, v, w)
+                                  : levels == 2 ? rs::piece_offsets<2>(d, v, w)
+                                                : rs::piece_offsets<3>(d, v, w);
+            for (uint32_t r = 0; r < d.nfan; ++r) {
+                char *dst = static_cast<char *>(dst_ptrs[p->fan[d.fan_off + r]]);
+                std::memcpy(dst + o.dst, src + o.src, w);
+            }
+        }
+    }
+    return RESHARD_OK;
+}
+
+const char *reshard_last_error(void) { return rs::g_last_error.c_str(); }
+
+const char *reshard_version(void) { return "0.1.0"; }
+
+}  // extern "C"

@@ -1,0 +1,95 @@
+// desc.h -- descriptor table the resharding kernel runs from.
+//
+// One descriptor is one workgroup's chunk of work: a range of W-byte vectors
+// inside a "piece", where a piece is part of one unit task's slice seen as
+//   (outer level 3) x (outer level 2) x (outer level 1) x (run of vpr vectors)
+// with independent byte strides on the sender side and the receiver side.
+// The run is contiguous in both buffers.  The sender buffer is read once and
+// every receiver gets the same bytes at the same local offset (replicas of a
+// destination slice share one local layout).
+//
+// Index arithmetic uses division by invariant integers through a multiply and
+// shift (Granlund & Montgomery, "Division by invariant integers using
+// multiplication", PLDI 1994, the round-up method for N = 32): for a divisor
+// d in [1, 2^31] let l = ceil(log2 d) and m = floor(2^32 (2^l - d) / d) + 1;
+// then floor(n / d) = (mulhi(m, n) + n) >> l for every 32-bit n.
+// The helpers are constexpr so the same code serves host and device.
+#pragma once
+
+#include <stdint.h>
+
+namespace rs {
+
+struct FastDiv {
+    uint32_t mul;
+    uint32_t shift;
+};
+
+constexpr FastDiv make_fastdiv(uint32_t d) {
+    uint32_t l = 0;
+    while ((uint64_t(1) << l) < d) ++l;
+    const uint64_t m = ((uint64_t(1) << 32) * ((uint64_t(1) << l) - d)) / d + 1;
+    return FastDiv{uint32_t(m), l};
+}
+
+constexpr uint32_t fastdiv(uint32_t n, uint32_t mul, uint32_t shift) {
+    const uint64_t t = (uint64_t(mul) * n) >> 32;
+    return uint32_t((t + n) >> shift);
+}
+
+// Kernel variant: log2 of the vector width and the number of outer levels.
+constexpr uint32_t make_kind(uint32_t log2w, uint32_t levels) { return log2w | (levels << 4); }
+constexpr uint32_t kind_log2w(uint32_t kind) { return kind & 0xFu; }
+constexpr uint32_t kind_levels(uint32_t kind) { return kind >> 4; }
+
+struct alignas(16) Desc {
+    uint64_t src_off;    // byte offset of the piece origin in the sender buffer
+    uint64_t dst_off;    // byte offset of the piece origin in every receiver buffer
+    int64_t ss[3];       // sender byte strides of outer levels 1..3 (1 = innermost)
+    int64_t ds[3];       // receiver byte strides of outer levels 1..3
+    uint32_t v0, v1;     // this chunk: vectors [v0, v1) of the piece
+    uint32_t vpr;        // vectors per run
+    uint32_t n1, n2;     // extents of outer levels 1 and 2 (level 3 is bounded by v1)
+    uint32_t mul_vpr, mul_n1, mul_n2;  // fast-division multipliers
+    uint8_t sh_vpr, sh_n1, sh_n2;      // fast-division shifts
+    uint8_t kind;        // make_kind(log2 W, levels), levels in 1..3
+    uint16_t src_buf;    // sender: index into the source pointer table
+    uint16_t nfan;       // number of receivers
+    uint32_t fan_off;    // receivers: fan[fan_off .. fan_off + nfan) index the dst table
+};
+static_assert(sizeof(Desc) == 112, "descriptor layout is shared by host and device");
+
+// Byte offsets (sender, receiver) of vector v of a descriptor's piece.
+struct Offsets {
+    uint64_t src;
+    uint64_t dst;
+};
+
+template <int LEVELS>
+constexpr Offsets piece_offsets(const Desc &d, uint32_t v, uint32_t vbytes) {
+    const uint32_t row = fastdiv(v, d.mul_vpr, d.sh_vpr);
+    const uint32_t col = v - row * d.vpr;
+    uint64_t s = uint64_t(col) * vbytes;
+    uint64_t t = s;
+    if (LEVELS == 1) {
+        s += uint64_t(row) * uint64_t(d.ss[0]);
+        t += uint64_t(row) * uint64_t(d.ds[0]);
+    } else {
+        const uint32_t r2 = fastdiv(row, d.mul_n1, d.sh_n1);
+        const uint32_t r1 = row - r2 * d.n1;
+        s += uint64_t(r1) * uint64_t(d.ss[0]);
+        t += uint64_t(r1) * uint64_t(d.ds[0]);
+        if (LEVELS == 2) {
+            s += uint64_t(r2) * uint64_t(d.ss[1]);
+            t += uint64_t(r2) * uint64_t(d.ds[1]);
+        } else {
+            const uint32_t r3 = fastdiv(r2, d.mul_n2, d.sh_n2);
+            const uint32_t q2 = r2 - r3 * d.n2;
+            s += uint64_t(q2) * uint64_t(d.ss[1]) + uint64_t(r3) * uint64_t(d.ss[2]);
+            t += uint64_t(q2) * uint64_t(d.ds[1]) + uint64_t(r3) * uint64_t(d.ds[2]);
+        }
+    }
+    return Offsets{s + d.src_off, t + d.dst_off};
+}
+
+}  // namespace rs

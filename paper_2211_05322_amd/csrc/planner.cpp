@@ -1,0 +1,439 @@
+// planner.cpp -- host planning of a cross-mesh resharding task (no HIP calls).
+#include "planner.hpp"
+
+#include <algorithm>
+#include <numeric>
+
+namespace rs {
+
+// ---------------------------------------------------------------- parsing
+// Section 2.2, "Sharding spec": one letter per tensor dim, R or S with the
+// mesh dims the tensor dim is split along.  Accepts S^0, S_0, S^{01}, S01.
+std::string parse_spec(const char *spec, int ndim, int mesh_ndim, std::vector<std::vector<int>> &axes) {
+    axes.clear();
+    if (!spec) return "spec is NULL";
+    const std::string s(spec);
+    size_t i = 0;
+    auto skip = [&]() { while (i < s.size() && (s[i] == ' ' || s[i] == ',' || s[i] == '\t')) ++i; };
+    skip();
+    while (i < s.size()) {
+        const char c = s[i];
+        if (c == 'R') {
+            axes.emplace_back();
+            ++i;
+        } else if (c == 'S') {
+            ++i;
+            if (i < s.size() && (s[i] == '^' || s[i] == '_')) ++i;
+            bool brace = false;
+            if (i < s.size() && s[i] == '{') { brace = true; ++i; }
+            std::vector<int> a;
+            while (i < s.size() && s[i] >= '0' && s[i] <= '9') a.push_back(s[i++] - '0');
+            if (a.empty()) return "spec '" + s + "': S without mesh axes";
+            if (brace) {
+                if (i >= s.size() || s[i] != '}') return "spec '" + s + "': missing '}'";
+                ++i;
+            }
+            axes.push_back(std::move(a));
+        } else {
+            return "spec '" + s + "': unexpected character '" + std::string(1, c) + "'";
+        }
+        skip();
+    }
+    if (int(axes.size()) != ndim)
+        return "spec '" + s + "' has " + std::to_string(axes.size()) + " letters but the tensor has " +
+               std::to_string(ndim) + " dims";
+    std::vector<int> used(10, 0);
+    for (auto &a : axes)
+        for (int x : a) {
+            if (x >= mesh_ndim)
+                return "spec '" + s + "' names mesh axis " + std::to_string(x) + " but the mesh has " +
+                       std::to_string(mesh_ndim) + " axes";
+            if (used[x]++) return "spec '" + s + "' uses mesh axis " + std::to_string(x) + " twice";
+        }
+    return "";
+}
+
+// ----------------------------------------------------------------- layout
+std::string build_layout(const std::vector<int64_t> &shape, const std::vector<int64_t> &mesh,
+                         const std::vector<std::vector<int>> &axes, Layout &L) {
+    const int nd = int(shape.size());
+    L.mesh = mesh;
+    L.axes = axes;
+    L.ndev = 1;
+    for (int64_t m : mesh) L.ndev *= m;
+    L.nshards.assign(nd, 1);
+    L.bounds.assign(nd, {});
+    for (int d = 0; d < nd; ++d) {
+        int64_t k = 1;
+        for (int a : axes[d]) k *= mesh[a];
+        L.nshards[d] = k;
+        // balanced split: the first (l mod k) shards are one element longer
+        const int64_t l = shape[d], q = l / k, r = l % k;
+        auto &b = L.bounds[d];
+        b.resize(k + 1);
+        for (int64_t j = 0; j <= k; ++j) b[j] = j * q + std::min(j, r);
+    }
+    // device -> shard index per dim (row-major device numbering; axis list major to minor)
+    const int md = int(mesh.size());
+    L.dev_shard.assign(L.ndev * nd, 0);
+    std::vector<int64_t> c(md);
+    for (int64_t dev = 0; dev < L.ndev; ++dev) {
+        int64_t rem = dev;
+        for (int a = md - 1; a >= 0; --a) { c[a] = rem % mesh[a]; rem /= mesh[a]; }
+        for (int d = 0; d < nd; ++d) {
+            int64_t j = 0;
+            for (int a : axes[d]) j = j * mesh[a] + c[a];
+            L.dev_shard[dev * nd + d] = j;
+        }
+    }
+    // CSR: linearised shard tuple -> holders
+    int64_t nlin = 1;
+    for (int d = 0; d < nd; ++d) nlin *= L.nshards[d];
+    std::vector<int64_t> lin(L.ndev);
+    L.shard_devs_off.assign(nlin + 1, 0);
+    for (int64_t dev = 0; dev < L.ndev; ++dev) {
+        int64_t x = 0;
+        for (int d = 0; d < nd; ++d) x = x * L.nshards[d] + L.dev_shard[dev * nd + d];
+        lin[dev] = x;
+        L.shard_devs_off[x + 1]++;
+    }
+    for (int64_t x = 0; x < nlin; ++x) L.shard_devs_off[x + 1] += L.shard_devs_off[x];
+    L.shard_devs.assign(L.ndev, 0);
+    std::vector<int64_t> fill(L.shard_devs_off.begin(), L.shard_devs_off.end() - 1);
+    for (int64_t dev = 0; dev < L.ndev; ++dev) L.shard_devs[fill[lin[dev]]++] = int32_t(dev);
+    return "";
+}
+
+// ------------------------------------------------------------- unit tasks
+namespace {
+struct Overlap {
+    int64_t lo, hi, js, jd;
+};
+}  // namespace
+
+void build_tasks(Plan &p) {
+    const int nd = p.ndim;
+    std::vector<std::vector<Overlap>> per(nd);
+    for (int d = 0; d < nd; ++d) {
+        const auto &bs = p.src.bounds[d], &bd = p.dst.bounds[d];
+        const int64_t ks = p.src.nshards[d], kd = p.dst.nshards[d];
+        int64_t i = 0, j = 0;
+        while (i < ks && j < kd) {
+            const int64_t lo = std::max(bs[i], bd[j]), hi = std::min(bs[i + 1], bd[j + 1]);
+            if (lo < hi) per[d].push_back({lo, hi, i, j});
+            if (bs[i + 1] <= bd[j + 1]) ++i; else ++j;
+        }
+    }
+    p.tasks.clear();
+    for (int d = 0; d < nd; ++d)
+        if (per[d].empty()) return;
+    std::vector<size_t> idx(nd, 0);
+    for (;;) {
+        UnitTask t;
+        t.lo.resize(nd);
+        t.hi.resize(nd);
+        int64_t vol = 1, xs = 0, xd = 0;
+        for (int d = 0; d < nd; ++d) {
+            const Overlap &o = per[d][idx[d]];
+            t.lo[d] = o.lo;
+            t.hi[d] = o.hi;
+            vol *= o.hi - o.lo;
+            xs = xs * p.src.nshards[d] + o.js;
+            xd = xd * p.dst.nshards[d] + o.jd;
+        }
+        t.src_shard = xs;
+        t.dst_shard = xd;
+        t.bytes = vol * p.es;
+        p.tasks.push_back(std::move(t));
+        int d = nd - 1;
+        while (d >= 0 && ++idx[d] == per[d].size()) idx[d--] = 0;
+        if (d < 0) break;
+    }
+}
+
+// ----------------------------------------------------------- sender choice
+void choose_senders(Plan &p) {
+    const auto &off = p.src.shard_devs_off;
+    const auto &devs = p.src.shard_devs;
+    if (p.flags & 0x1u) {  // naive: lowest-indexed owner
+        for (auto &t : p.tasks) t.sender = devs[off[t.src_shard]];
+        return;
+    }
+    // Eq. 4: tasks longest first (ties keep task order), each to the owner
+    // with the least bytes assigned so far (ties: lowest device index).
+    std::vector<size_t> order(p.tasks.size());
+    std::iota(order.begin(), order.end(), size_t(0));
+    std::stable_sort(order.begin(), order.end(),
+                     [&](size_t a, size_t b) { return p.tasks[a].bytes > p.tasks[b].bytes; });
+    std::vector<int64_t> load(p.src.ndev, 0);
+    for (size_t i : order) {
+        auto &t = p.tasks[i];
+        int32_t best = -1;
+        for (int64_t k = off[t.src_shard]; k < off[t.src_shard + 1]; ++k) {
+            const int32_t dev = devs[k];  // ascending, so strict < keeps the lowest index on ties
+            if (best < 0 || load[dev] < load[best]) best = dev;
+        }
+        t.sender = best;
+        load[best] += t.bytes;
+    }
+}
+
+// ---------------------------------------------------------------- lowering
+namespace {
+
+struct Level {
+    int64_t n, ss, ds;  // extent, sender byte stride, receiver byte stride
+};
+
+struct Piece {
+    uint64_t src_off, dst_off;
+    int64_t run;               // bytes, contiguous on both sides
+    std::vector<Level> outer;  // outermost first, at most 3
+    int32_t w;                 // vector bytes
+};
+
+int64_t pow2_divisor(int64_t x, int64_t cap) {
+    int64_t w = cap;
+    while (w > 1 && (x % w) != 0) w >>= 1;
+    return w;
+}
+
+int32_t pick_width(uint64_t so, uint64_t dso, int64_t run, const std::vector<Level> &outer) {
+    int64_t w = 16;
+    w = pow2_divisor(int64_t(so), w);
+    w = pow2_divisor(int64_t(dso), w);
+    w = pow2_divisor(run, w);
+    for (const auto &l : outer) {
+        w = pow2_divisor(l.ss, w);
+        w = pow2_divisor(l.ds, w);
+    }
+    return int32_t(w);
+}
+
+constexpr uint64_t kMaxPieceVectors = (uint64_t(1) << 31) - 1;
+constexpr uint64_t kMaxDescs = uint64_t(1) << 24;  // 1.75 GiB of descriptors
+
+// Emit chunks of a piece whose outer list has at most 3 levels and fewer
+// than 2^31 vectors.
+void emit(Plan &p, const Piece &pc, int32_t src_buf, int64_t fan_off, int64_t nfan, int64_t chunk_bytes) {
+    Desc d{};
+    d.src_off = pc.src_off;
+    d.dst_off = pc.dst_off;
+    const int nl = int(pc.outer.size());
+    const int levels = std::max(1, nl);
+    // outer[] is outermost first; Desc level 1 is the innermost outer level
+    for (int i = 0; i < nl; ++i) {
+        const Level &l = pc.outer[nl - 1 - i];
+        d.ss[i] = l.ss;
+        d.ds[i] = l.ds;
+    }
+    const uint64_t vpr = uint64_t(pc.run / pc.w);
+    uint64_t rows = 1;
+    for (const auto &l : pc.outer) rows *= uint64_t(l.n);
+    const uint64_t total = vpr * rows;
+    d.vpr = uint32_t(vpr);
+    d.n1 = nl >= 2 ? uint32_t(pc.outer[nl - 1].n) : 1u;
+    d.n2 = nl >= 3 ? uint32_t(pc.outer[nl - 2].n) : 1u;
+    const FastDiv f0 = make_fastdiv(d.vpr), f1 = make_fastdiv(d.n1), f2 = make_fastdiv(d.n2);
+    d.mul_vpr = f0.mul; d.sh_vpr = uint8_t(f0.shift);
+    d.mul_n1 = f1.mul;  d.sh_n1 = uint8_t(f1.shift);
+    d.mul_n2 = f2.mul;  d.sh_n2 = uint8_t(f2.shift);
+    uint32_t log2w = 0;
+    while ((1 << log2w) < pc.w) ++log2w;
+    d.kind = uint8_t(make_kind(log2w, uint32_t(levels)));
+    d.src_buf = uint16_t(src_buf);
+    d.nfan = uint16_t(nfan);
+    d.fan_off = uint32_t(fan_off);
+    // chunk length in vectors: whole 256-byte groups where the width allows
+    uint64_t cv = uint64_t(std::max<int64_t>(1, chunk_bytes / pc.w));
+    const uint64_t grain = uint64_t(256 / pc.w);
+    cv = std::max(grain, cv / grain * grain);
+    if (p.descs.size() + (total + cv - 1) / cv > kMaxDescs) {
+        p.too_many = true;
+        return;
+    }
+    for (uint64_t v0 = 0; v0 < total; v0 += cv) {
+        d.v0 = uint32_t(v0);
+        d.v1 = uint32_t(std::min(total, v0 + cv));
+        p.descs.push_back(d);
+    }
+    p.align = std::max<int64_t>(p.align, pc.w);
+}
+
+// Emit every row of the outermost level as its own piece (level removed).
+void split_emit(Plan &p, Piece pc, int32_t src_buf, int64_t fan_off, int64_t nfan, int64_t chunk_bytes);
+
+void peel_top(Plan &p, const Piece &pc, int32_t src_buf, int64_t fan_off, int64_t nfan, int64_t chunk_bytes) {
+    const Level top = pc.outer.front();
+    Piece sub = pc;
+    sub.outer.erase(sub.outer.begin());
+    for (int64_t i = 0; i < top.n; ++i) {
+        sub.src_off = pc.src_off + uint64_t(i * top.ss);
+        sub.dst_off = pc.dst_off + uint64_t(i * top.ds);
+        split_emit(p, sub, src_buf, fan_off, nfan, chunk_bytes);
+    }
+}
+
+// Split a piece until it has at most 3 outer levels and fewer than 2^31
+// vectors, then emit it.
+void split_emit(Plan &p, Piece pc, int32_t src_buf, int64_t fan_off, int64_t nfan, int64_t chunk_bytes) {
+    if (p.too_many) return;
+    if (pc.outer.size() > 3) {
+        peel_top(p, pc, src_buf, fan_off, nfan, chunk_bytes);
+        return;
+    }
+    uint64_t rows = 1;
+    for (const auto &l : pc.outer) rows *= uint64_t(l.n);
+    const uint64_t vpr = uint64_t(pc.run / pc.w);
+    const uint64_t total = vpr * rows;
+    if (total <= kMaxPieceVectors) {
+        emit(p, pc, src_buf, fan_off, nfan, chunk_bytes);
+        return;
+    }
+    if (pc.outer.empty()) {
+        // a single run longer than the index range: cut it into segments
+        const int64_t segb = (int64_t(1) << 30) * pc.w;
+        for (int64_t b = 0; b < pc.run; b += segb) {
+            Piece sub = pc;
+            sub.run = std::min(segb, pc.run - b);
+            sub.src_off = pc.src_off + uint64_t(b);
+            sub.dst_off = pc.dst_off + uint64_t(b);
+            emit(p, sub, src_buf, fan_off, nfan, chunk_bytes);
+        }
+        return;
+    }
+    const Level top = pc.outer.front();
+    const uint64_t inner = total / uint64_t(top.n);
+    if (inner > kMaxPieceVectors) {
+        peel_top(p, pc, src_buf, fan_off, nfan, chunk_bytes);
+        return;
+    }
+    // cut the outermost level into ranges that fit
+    const int64_t step = int64_t(kMaxPieceVectors / inner);
+    for (int64_t i = 0; i < top.n; i += step) {
+        Piece sub = pc;
+        sub.outer.front().n = std::min(step, top.n - i);
+        sub.src_off = pc.src_off + uint64_t(i * top.ss);
+        sub.dst_off = pc.dst_off + uint64_t(i * top.ds);
+        emit(p, sub, src_buf, fan_off, nfan, chunk_bytes);
+    }
+}
+
+int64_t auto_chunk_bytes(int64_t bytes_read) {
+    // Enough chunks to fill 256 CUs several times over, 4 KiB .. 64 KiB each.
+    int64_t c = 4096;
+    while (c < 65536 && bytes_read / (2 * c) >= 4096) c *= 2;
+    return c;
+}
+
+}  // namespace
+
+void lower(Plan &p) {
+    const int nd = p.ndim;
+    const int64_t es = p.es;
+    p.descs.clear();
+    p.fan.assign(p.dst.shard_devs.begin(), p.dst.shard_devs.end());
+    p.align = 1;
+    p.too_many = false;
+    p.max_fanout = 0;
+    p.bytes_read = 0;
+    for (const auto &t : p.tasks) p.bytes_read += t.bytes;
+    const int64_t chunk = p.tuning.chunk_bytes > 0 ? p.tuning.chunk_bytes : auto_chunk_bytes(p.bytes_read);
+
+    std::vector<int64_t> ext_s(nd), ext_d(nd), str_s(nd), str_d(nd);
+    for (const auto &t : p.tasks) {
+        const int64_t fan_off = p.dst.shard_devs_off[t.dst_shard];
+        const int64_t nfan = p.dst.shard_devs_off[t.dst_shard + 1] - fan_off;
+        p.max_fanout = std::max(p.max_fanout, nfan);
+        const int32_t rcv0 = p.dst.shard_devs[fan_off];
+        // local boxes of the sender and of (any) receiver
+        uint64_t so = 0, dso = 0;
+        for (int d = 0; d < nd; ++d) {
+            const int64_t js = p.src.dev_shard[int64_t(t.sender) * nd + d];
+            const int64_t jd = p.dst.dev_shard[int64_t(rcv0) * nd + d];
+            ext_s[d] = p.src.bounds[d][js + 1] - p.src.bounds[d][js];
+            ext_d[d] = p.dst.bounds[d][jd + 1] - p.dst.bounds[d][jd];
+        }
+        int64_t a = es, b = es;
+        for (int d = nd - 1; d >= 0; --d) {
+            str_s[d] = a;
+            str_d[d] = b;
+            a *= ext_s[d];
+            b *= ext_d[d];
+        }
+        for (int d = 0; d < nd; ++d) {
+            const int64_t js = p.src.dev_shard[int64_t(t.sender) * nd + d];
+            const int64_t jd = p.dst.dev_shard[int64_t(rcv0) * nd + d];
+            so += uint64_t((t.lo[d] - p.src.bounds[d][js]) * str_s[d]);
+            dso += uint64_t((t.lo[d] - p.dst.bounds[d][jd]) * str_d[d]);
+        }
+        // collapse: drop unit extents, merge dims contiguous on both sides
+        std::vector<Level> g;  // innermost first while building
+        for (int d = nd - 1; d >= 0; --d) {
+            const int64_t n = t.hi[d] - t.lo[d];
+            if (n == 1) continue;
+            if (!g.empty() && str_s[d] == g.back().n * g.back().ss && str_d[d] == g.back().n * g.back().ds)
+                g.back().n *= n;
+            else
+                g.push_back({n, str_s[d], str_d[d]});
+        }
+        int64_t run = es;
+        if (!g.empty() && g.front().ss == es && g.front().ds == es) {
+            run = g.front().n * es;
+            g.erase(g.begin());
+        }
+        std::reverse(g.begin(), g.end());  // outermost first
+
+        // Head / body / tail split so the body moves whole 16-byte vectors
+        // when both sides share the 16-byte phase on every row.
+        bool phase_ok = ((so - dso) % 16) == 0;
+        for (const auto &l : g) phase_ok = phase_ok && (l.ss % 16 == 0) && (l.ds % 16 == 0);
+        std::vector<Piece> parts;
+        if (phase_ok && run >= 32) {
+            const int64_t head = std::min<int64_t>(run, int64_t((16 - so % 16) % 16));
+            const int64_t body = (run - head) / 16 * 16;
+            const int64_t tail = run - head - body;
+            int64_t at = 0;
+            for (int64_t len : {head, body, tail}) {
+                if (len > 0) {
+                    Piece pc{so + uint64_t(at), dso + uint64_t(at), len, g, 1};
+                    pc.w = pick_width(pc.src_off, pc.dst_off, pc.run, pc.outer);
+                    parts.push_back(pc);
+                }
+                at += len;
+            }
+        } else {
+            Piece pc{so, dso, run, g, 1};
+            pc.w = pick_width(so, dso, run, g);
+            parts.push_back(pc);
+        }
+        for (const auto &pc : parts) split_emit(p, pc, t.sender, fan_off, nfan, chunk);
+    }
+    p.bytes_written = 0;
+    p.dst_local_numel.assign(p.dst.ndev, 0);
+    p.src_local_numel.assign(p.src.ndev, 0);
+    std::vector<int64_t> shp(nd);
+    for (int64_t dev = 0; dev < p.dst.ndev; ++dev) {
+        local_shape(p, 1, dev, shp.data());
+        int64_t n = 1;
+        for (int64_t x : shp) n *= x;
+        p.dst_local_numel[dev] = n;
+        p.bytes_written += n * es;
+    }
+    for (int64_t dev = 0; dev < p.src.ndev; ++dev) {
+        local_shape(p, 0, dev, shp.data());
+        int64_t n = 1;
+        for (int64_t x : shp) n *= x;
+        p.src_local_numel[dev] = n;
+    }
+}
+
+void local_shape(const Plan &p, int side, int64_t dev, int64_t *out) {
+    const Layout &L = side == 0 ? p.src : p.dst;
+    for (int d = 0; d < p.ndim; ++d) {
+        const int64_t j = L.dev_shard[dev * p.ndim + d];
+        out[d] = L.bounds[d][j + 1] - L.bounds[d][j];
+    }
+}
+
+}  // namespace rs

@@ -1,0 +1,83 @@
+// planner.hpp -- host-side planning of one cross-mesh resharding task.
+//
+// Steps (all host, no HIP):
+//   parse      spec strings -> mesh axes per tensor dimension (Section 2.2)
+//   layout     device -> shard index per dimension, shard bounds per dimension
+//   tasks      unit tasks = non-empty intersections of a source shard and a
+//              destination shard, with all owners and all receivers
+//              (Section 2.2; the same slices as the appendix cut-point
+//              decomposition, computed here dimension by dimension as
+//              intersections of shard intervals)
+//   senders    one owner per task: naive (lowest index) or longest-first
+//              greedy balancing of sent bytes (Section 3.2, Eq. 4)
+//   lowering   each task -> pieces (collapsed strided boxes) -> chunks
+//              (descriptors, one per workgroup)
+#pragma once
+
+#include <cstdint>
+#include <mutex>
+#include <string>
+#include <vector>
+
+#include "desc.h"
+
+namespace rs {
+
+struct Layout {
+    std::vector<int64_t> mesh;               // mesh shape
+    std::vector<std::vector<int>> axes;      // per tensor dim: mesh axes, major to minor
+    std::vector<int64_t> nshards;            // per tensor dim
+    std::vector<std::vector<int64_t>> bounds;  // per dim: nshards+1 cut positions
+    int64_t ndev = 0;
+    std::vector<int64_t> dev_shard;          // [dev * ndim + dim] -> shard index
+    std::vector<int64_t> shard_devs_off;     // CSR over linearised shard tuples
+    std::vector<int32_t> shard_devs;         //   -> devices holding that shard (ascending)
+};
+
+struct UnitTask {
+    std::vector<int64_t> lo, hi;   // slice of D
+    int64_t src_shard = 0;         // linearised source shard tuple
+    int64_t dst_shard = 0;         // linearised destination shard tuple
+    int64_t bytes = 0;
+    int32_t sender = -1;           // chosen owner
+};
+
+struct Tuning {
+    int64_t chunk_bytes = 0;   // 0: automatic
+    int32_t block_threads = 256;
+};
+
+struct Plan {
+    int ndim = 0;
+    std::vector<int64_t> shape;
+    int64_t es = 0;            // element size in bytes
+    unsigned flags = 0;
+    Tuning tuning;
+    Layout src, dst;
+    std::vector<UnitTask> tasks;
+    std::vector<Desc> descs;
+    std::vector<int32_t> fan;  // receiver lists, referenced by Desc::fan_off/nfan
+    int64_t bytes_read = 0, bytes_written = 0, max_fanout = 0;
+    int64_t align = 1;         // required buffer alignment in bytes
+    bool too_many = false;     // lowering stopped: descriptor table over its cap
+    std::vector<int64_t> src_local_numel, dst_local_numel;  // per device
+
+    // Device copy of [descs | fan], uploaded on the first execute on each HIP
+    // device (index = device ordinal).
+    static constexpr int kMaxHipDevices = 64;
+    mutable std::mutex mu;
+    mutable void *d_table[kMaxHipDevices] = {};
+};
+
+// Returns "" on success, else an error message; `code` receives the status.
+std::string parse_spec(const char *spec, int ndim, int mesh_ndim, std::vector<std::vector<int>> &axes);
+std::string build_layout(const std::vector<int64_t> &shape, const std::vector<int64_t> &mesh,
+                         const std::vector<std::vector<int>> &axes, Layout &out);
+void build_tasks(Plan &p);
+void choose_senders(Plan &p);
+void lower(Plan &p);
+
+// Local (per-device) shape on one side.
+void local_shape(const Plan &p, int side, int64_t dev, int64_t *out);
+
+}  // namespace rs

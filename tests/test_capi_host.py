@@ -1,0 +1,260 @@
+"""C-ABI checks that need no GPU: exports, planning, errors, host interpreter.
+
+The planner's unit tasks, senders, local shapes and traffic totals are
+compared exactly with the oracle; the descriptor table is run on host
+memory by reshard_debug_execute_host and compared bit for bit with the
+oracle's destination shards (guard bytes around every buffer must stay
+untouched).  No kernel runs here.
+"""
+
+import ctypes
+import os
+import random
+import re
+
+import numpy as np
+import pytest
+
+import oracle
+from paper_2211_05322_amd import binding as B
+from paper_2211_05322_amd.workloads import WORKLOADS
+from tests.test_oracle_pins import fmt_spec, random_dims
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "reshard.h")
+
+_NP = {"float16": np.float16, "float32": np.float32, "uint8": np.uint8, "float64": np.float64,
+       "int16": np.int16, "int32": np.int32, "int64": np.int64, "bfloat16": np.uint16}
+
+
+def declared_functions():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(reshard_[a-z_]+)\s*\(", text)))
+
+
+def test_library_exports_every_declared_symbol():
+    lib = B.load()
+    names = declared_functions()
+    assert {"reshard_plan", "reshard_execute", "reshard_plan_destroy", "reshard_plan_local_shape",
+            "reshard_plan_stats", "reshard_last_error"} <= set(names)
+    for n in names:
+        assert hasattr(lib, n), n
+    assert B.reshard_version() == "0.1.0"
+
+
+def plan_of(shape, dtype, sm, ss, dm, ds, **kw):
+    return B.reshard_plan(shape, dtype, sm, ss, dm, ds, **kw)
+
+
+def check_against_oracle(shape, dtype, sm, ss, dm, ds, flags=0, itemsize=None):
+    p = plan_of(shape, dtype, sm, ss, dm, ds, flags=flags)
+    es = itemsize or np.dtype(_NP[dtype]).itemsize
+    tasks = oracle.unit_tasks(shape, sm, ss, dm, ds)
+    st = B.reshard_plan_stats(p)
+    assert st["n_unit_tasks"] == len(tasks)
+    rd, wr = oracle.traffic_bytes(shape, es, dm, ds)
+    assert (st["bytes_read"], st["bytes_written"]) == (rd, wr)
+    if flags & B.RESHARD_SENDER_NAIVE:
+        chosen = oracle.choose_senders_naive(tasks)
+    else:
+        chosen = oracle.choose_senders_lpt(tasks, es, int(np.prod(sm)))
+    for i, t in enumerate(tasks):
+        got = B.reshard_plan_unit_task(p, i)
+        assert got["box"] == t["box"]
+        assert got["senders"] == t["senders"]
+        assert got["receivers"] == t["receivers"]
+        assert got["sender"] == chosen[i]
+    for side, mesh, spec in ((0, sm, ss), (1, dm, ds)):
+        for k in range(int(np.prod(mesh))):
+            assert B.reshard_plan_local_shape(p, side, k) == oracle.local_shape(shape, mesh, spec, k)
+    return p
+
+
+# ----------------------------------------------------------------- planning
+
+def test_fig2_plans():
+    check_against_oracle((4, 4), "float32", (2, 2), "S^{01}R", (2, 2), "S^0R")
+    check_against_oracle((4, 4), "float32", (2, 2), "S^0R", (2, 2), "S^0R")
+
+
+@pytest.mark.parametrize("case", range(1, 10))
+@pytest.mark.parametrize("flags", [0, B.RESHARD_SENDER_NAIVE])
+def test_table3_plans_full_size(case, flags):
+    import json
+    g = json.load(open(os.path.join(ROOT, "tests", "golden", "table3_cases.json")))
+    c = g["cases"][case - 1]
+    check_against_oracle(tuple(g["tensor_shape"]), "float16", tuple(c["send_mesh"]), c["send_spec"],
+                         tuple(c["recv_mesh"]), c["recv_spec"], flags=flags)
+
+
+@pytest.mark.parametrize("wid", sorted(WORKLOADS))
+def test_workload_plans(wid):
+    w = WORKLOADS[wid]
+    p = check_against_oracle(w.shape, w.dtype, w.src_mesh, w.src_spec, w.dst_mesh, w.dst_spec)
+    st = B.reshard_plan_stats(p)
+    assert B.reshard_plan_alignment(p) == 16  # every workload takes the 16-byte path
+    assert st["max_fanout"] == {1: 2, 2: 1, 3: 8, 4: 2, 5: 4}[wid]
+
+
+def _fuzz(n, seed, max_len=12):
+    rng = random.Random(seed)
+    out = []
+    while len(out) < n:
+        ndim = rng.randint(1, 5)
+        shape = tuple(rng.randint(0, max_len) if rng.random() < 0.05 else rng.randint(1, max_len)
+                      for _ in range(ndim))
+        sm = tuple(rng.randint(1, 4) for _ in range(rng.randint(1, 3)))
+        dm = tuple(rng.randint(1, 4) for _ in range(rng.randint(1, 3)))
+        out.append((shape, rng.choice(["uint8", "float16", "float32", "float64"]), sm,
+                    fmt_spec(random_dims(rng, ndim, len(sm))), dm, fmt_spec(random_dims(rng, ndim, len(dm))),
+                    rng.choice([0, 0, B.RESHARD_SENDER_NAIVE])))
+    return out
+
+
+@pytest.mark.parametrize("case", _fuzz(60, 5))
+def test_fuzz_plans(case):
+    shape, dt, sm, ss, dm, ds, flags = case
+    check_against_oracle(shape, dt, sm, ss, dm, ds, flags=flags)
+
+
+# -------------------------------------------------------- host interpreter
+
+GUARD = 64
+
+
+def run_host(p, src_arrays, dst_shapes, np_dtype):
+    """Execute the descriptor table on host buffers with guard bands."""
+    es = np.dtype(np_dtype).itemsize
+    srcs = []
+    for a in src_arrays:
+        raw = np.full(a.nbytes + 2 * GUARD, 0xA5, dtype=np.uint8)
+        raw[GUARD:GUARD + a.nbytes] = np.ascontiguousarray(a).view(np.uint8).ravel()
+        srcs.append(raw)
+    dsts = [np.full(int(np.prod(s)) * es + 2 * GUARD, 0x5A, dtype=np.uint8) for s in dst_shapes]
+    # 16-byte aligned views one guard band in
+    sp = [r.ctypes.data + GUARD if r.size > 2 * GUARD else None for r in srcs]
+    dp = [r.ctypes.data + GUARD if r.size > 2 * GUARD else None for r in dsts]
+    for q in sp + dp:
+        assert q is None or q % 16 == 0
+    B.load().reshard_debug_execute_host(p.handle, B._ptrs(sp), B._ptrs(dp))
+    outs = []
+    for r, s in zip(dsts, dst_shapes):
+        assert (r[:GUARD] == 0x5A).all() and (r[r.size - GUARD:] == 0x5A).all(), "write outside buffer"
+        outs.append(r[GUARD:r.size - GUARD].view(np_dtype).reshape(s))
+    for r, a in zip(srcs, src_arrays):
+        assert (r[GUARD:GUARD + a.nbytes] == np.ascontiguousarray(a).view(np.uint8).ravel()).all()
+    return outs
+
+
+def host_case(shape, dt, sm, ss, dm, ds, flags=0, seed=0, **kw):
+    np_dtype = _NP[dt]
+    es = np.dtype(np_dtype).itemsize
+    rng = np.random.default_rng(seed)
+    x = rng.integers(0, 256, size=int(np.prod(shape)) * es, dtype=np.uint8).view(np_dtype).reshape(shape)
+    src = oracle.shard(x, sm, ss)
+    want = oracle.reshard(src, shape, sm, ss, dm, ds)
+    p = plan_of(shape, dt, sm, ss, dm, ds, flags=flags, **kw)
+    got = run_host(p, src, [w.shape for w in want], np_dtype)
+    for g, w in zip(got, want):
+        assert g.shape == w.shape
+        assert np.array_equal(g.view(f"u{es}"), w.view(f"u{es}"))
+
+
+@pytest.mark.parametrize("case", _fuzz(80, 11))
+def test_host_interpreter_fuzz(case):
+    shape, dt, sm, ss, dm, ds, flags = case
+    host_case(shape, dt, sm, ss, dm, ds, flags)
+
+
+@pytest.mark.parametrize("chunk", [0, 16, 48, 1000, 4096])
+@pytest.mark.parametrize("case", _fuzz(12, 23, max_len=40))
+def test_host_interpreter_chunking(case, chunk):
+    shape, dt, sm, ss, dm, ds, flags = case
+    host_case(shape, dt, sm, ss, dm, ds, flags, chunk_bytes=chunk)
+
+
+@pytest.mark.parametrize("wid", sorted(WORKLOADS))
+def test_host_interpreter_scaled_workloads(wid):
+    # the workload's meshes and specs on a shrunken tensor (every dim cut so
+    # splits stay exact or uneven as in the original)
+    w = WORKLOADS[wid]
+    small = {1: (64, 96), 2: (4, 64, 96), 3: (2, 24, 200), 4: (4, 8, 66, 16), 5: (2, 64, 384)}[wid]
+    host_case(small, w.dtype, w.src_mesh, w.src_spec, w.dst_mesh, w.dst_spec)
+
+
+def test_host_interpreter_misaligned_phase_and_long_runs():
+    # fp16 rows of odd length: source and destination 16-byte phases differ
+    host_case((3, 37, 29), "float16", (2, 2), "S^0S^1R", (3,), "RRS^0")
+    # long contiguous runs with a ragged tail
+    host_case((5, 1000), "float16", (1,), "RR", (2,), "RS^0")
+    # > 3 non-collapsible outer levels
+    host_case((3, 4, 3, 4, 3, 8), "uint8", (2, 2, 2), "RS^0RS^1RS^2", (2, 2), "S^0RS^1RRR")
+
+
+# ------------------------------------------------------------------ errors
+
+@pytest.mark.parametrize("args,status", [
+    (((4, 4), "float32", (2, 2), "S^0", (2, 2), "RR"), B.RESHARD_EINVAL),          # spec too short
+    (((4, 4), "float32", (2, 2), "S^2R", (2, 2), "RR"), B.RESHARD_EINVAL),         # axis outside mesh
+    (((4, 4), "float32", (2, 2), "S^0S^0", (2, 2), "RR"), B.RESHARD_EINVAL),       # axis reused
+    (((4, 4), "float32", (2, 2), "Q R", (2, 2), "RR"), B.RESHARD_EINVAL),          # bad letter
+    (((4, 4), "float32", (2, 2), "S^{0R", (2, 2), "RR"), B.RESHARD_EINVAL),        # missing brace
+    (((4, -1), "float32", (2, 2), "RR", (2, 2), "RR"), B.RESHARD_EINVAL),          # negative dim
+    (((4, 4), "float32", (2, 0), "RR", (2, 2), "RR"), B.RESHARD_EINVAL),           # empty mesh axis
+    (((4, 4), "float32", (16, 16), "RR", (16, 16), "RR"), B.RESHARD_EUNSUPPORTED),  # 512 buffers
+])
+def test_plan_errors(args, status):
+    with pytest.raises(B.ReshardError) as e:
+        plan_of(*args)
+    assert e.value.status == status
+    assert B.reshard_last_error()
+
+
+def test_plan_error_ndim_and_nulls():
+    lib = B.load()
+    h = ctypes.c_void_p()
+    shape = B._i64([2, 2])
+    mesh = B._i64([2])
+    assert lib.reshard_plan(0, shape, 2, 1, mesh, b"", 1, mesh, b"", 0, ctypes.byref(h)) == B.RESHARD_EINVAL
+    assert lib.reshard_plan(9, shape, 2, 1, mesh, b"R" * 9, 1, mesh, b"R" * 9, 0,
+                            ctypes.byref(h)) == B.RESHARD_EINVAL
+    assert lib.reshard_plan(2, None, 2, 1, mesh, b"RR", 1, mesh, b"RR", 0, ctypes.byref(h)) == B.RESHARD_EINVAL
+    assert lib.reshard_plan(2, shape, 2, 1, mesh, None, 1, mesh, b"RR", 0, ctypes.byref(h)) == B.RESHARD_EINVAL
+    assert lib.reshard_plan(2, shape, 2, 1, mesh, b"RR", 1, mesh, b"RR", 0, None) == B.RESHARD_EINVAL
+    assert lib.reshard_plan(2, shape, 99, 1, mesh, b"RR", 1, mesh, b"RR", 0, ctypes.byref(h)) == B.RESHARD_EINVAL
+    assert lib.reshard_plan(2, shape, 2, 1, mesh, b"RR", 1, mesh, b"RR", 0x80, ctypes.byref(h)) == B.RESHARD_EINVAL
+    assert lib.reshard_plan(2, shape, 2, 0, mesh, b"RR", 1, mesh, b"RR", 0, ctypes.byref(h)) == B.RESHARD_EINVAL
+    assert "1..8" in B.reshard_last_error()
+    lib.reshard_plan_destroy(None)  # NULL accepted
+    assert lib.reshard_execute(None, None, None, None) == B.RESHARD_EINVAL
+
+
+def test_query_errors():
+    p = plan_of((4, 4), "float16", (2,), "S^0R", (2,), "RS^0")
+    lib = B.load()
+    out = (ctypes.c_int64 * 2)()
+    assert lib.reshard_plan_local_shape(p.handle, 2, 0, out) == B.RESHARD_EINVAL
+    assert lib.reshard_plan_local_shape(p.handle, 0, 5, out) == B.RESHARD_EINVAL
+    assert lib.reshard_plan_unit_task(p.handle, 99, out, out, None, None, 0, None, None, 0, None) == B.RESHARD_EINVAL
+    with pytest.raises(B.ReshardError):
+        B.reshard_plan(( 4, 4), "float16", (2,), "RR", (2,), "RR", block_threads=100)
+
+
+def test_execute_rejects_null_buffer_on_host_interpreter():
+    p = plan_of((4, 4), "float16", (2,), "S^0R", (2,), "RS^0")
+    a = np.zeros((2, 4), np.float16)
+    with pytest.raises(B.ReshardError):
+        B.reshard_debug_execute_host(p, [a, None], [np.zeros((4, 2), np.float16)] * 2)
+
+
+def test_empty_tensor_and_empty_shards():
+    # zero-size tensor: no tasks, nothing to do
+    p = plan_of((0, 4), "float32", (2,), "S^0R", (2,), "RS^0")
+    st = B.reshard_plan_stats(p)
+    assert st["n_unit_tasks"] == 0 and st["n_descriptors"] == 0
+    B.reshard_debug_execute_host(p, [None, None], [None, None])
+    # 3 rows over 4 devices: the last shard is empty and may be NULL
+    host_case((3, 8), "float32", (4,), "S^0R", (2,), "RS^0")
+    p = plan_of((3, 8), "float32", (4,), "S^0R", (2,), "RS^0")
+    assert B.reshard_plan_local_shape(p, 0, 3) == (0, 8)

@@ -1,0 +1,233 @@
+"""GPU parity: the HIP kernel (through the C ABI) against the CPU oracle.
+
+Bit-exact comparison (raw bits) of every destination buffer.  Device
+buffers sit inside larger allocations with guard bands that must stay
+untouched.  Full-size workloads run in the launch configuration bench.py
+times (default plan options).
+"""
+
+import os
+import random
+
+import numpy as np
+import pytest
+import torch
+
+import oracle
+from paper_2211_05322_amd import binding as B
+from paper_2211_05322_amd.workloads import WORKLOADS, as_numpy_bits, make_workload_tensor
+from tests.test_capi_host import _fuzz
+from tests.test_oracle_pins import fmt_spec, random_dims
+
+pytestmark = pytest.mark.gpu
+
+GUARD = 256  # bytes on each side of every device buffer
+_T = {"uint8": torch.uint8, "float16": torch.float16, "float32": torch.float32, "float64": torch.float64,
+      "bfloat16": torch.bfloat16, "int16": torch.int16, "int32": torch.int32, "int64": torch.int64}
+
+
+def _say(msg):
+    print(msg, flush=True)
+
+
+class Guarded:
+    """A device buffer of `nbytes` inside an allocation with guard bands."""
+
+    def __init__(self, nbytes, fill):
+        self.nbytes = nbytes
+        self.raw = torch.full((nbytes + 2 * GUARD,), fill, dtype=torch.uint8, device="cuda")
+        self.fill = fill
+
+    @property
+    def ptr(self):
+        return self.raw.data_ptr() + GUARD if self.nbytes else None
+
+    def body(self):
+        return self.raw[GUARD:GUARD + self.nbytes]
+
+    def guards_ok(self):
+        return bool((self.raw[:GUARD] == self.fill).all()) and bool((self.raw[GUARD + self.nbytes:] == self.fill).all())
+
+
+def run_gpu(shape, dtype, sm, ss, dm, ds, x_cpu, flags=0, stream=None, **kw):
+    """Shard x on the host (oracle), run the kernel, return (got, want) raw-bit arrays."""
+    x = as_numpy_bits(x_cpu)
+    es = x.dtype.itemsize
+    src = oracle.shard(x, sm, ss)
+    want = oracle.reshard(src, shape, sm, ss, dm, ds)
+    p = B.reshard_plan(shape, dtype, sm, ss, dm, ds, flags=flags, **kw)
+    sbufs = []
+    for a in src:
+        g = Guarded(a.nbytes, 0xA5)
+        if a.nbytes:
+            g.body().copy_(torch.from_numpy(a.reshape(-1).view(np.uint8).copy()))
+        sbufs.append(g)
+    dbufs = [Guarded(w.nbytes, 0x5A) for w in want]
+    B.reshard_execute(p, [g.ptr for g in sbufs], [g.ptr for g in dbufs], stream=stream)
+    torch.cuda.synchronize()
+    got = []
+    for g, w in zip(dbufs, want):
+        assert g.guards_ok(), "kernel wrote outside a destination buffer"
+        got.append(g.body().cpu().numpy().view(f"u{es}").reshape(w.shape))
+    for g, a in zip(sbufs, src):
+        assert g.guards_ok()
+        if a.nbytes:
+            assert np.array_equal(g.body().cpu().numpy(), a.reshape(-1).view(np.uint8)), "source modified"
+    return got, want
+
+
+def assert_same(got, want):
+    assert len(got) == len(want)
+    for k, (g, w) in enumerate(zip(got, want)):
+        assert g.shape == w.shape, k
+        if not np.array_equal(g, w):
+            bad = np.argwhere(g != w)[:5]
+            raise AssertionError(f"buffer {k}: {int((g != w).sum())} elements differ, first at {bad.tolist()}")
+
+
+def rand_bits(shape, dtype, seed):
+    g = torch.Generator().manual_seed(seed)
+    es = torch.empty((), dtype=_T[dtype]).element_size()
+    n = int(np.prod(shape)) if shape else 1
+    raw = torch.randint(0, 256, (n * es,), generator=g, dtype=torch.uint8)
+    return raw.view(_T[dtype]).reshape(shape)
+
+
+def test_single_hip_runtime_in_process():
+    B.load()
+    torch.zeros(1, device="cuda")
+    maps = open("/proc/self/maps").read()
+    paths = {line.split()[-1] for line in maps.splitlines() if "libamdhip64" in line}
+    assert len(paths) == 1, paths
+
+
+def test_fig2_on_gpu():
+    _say("fig2")
+    x = torch.arange(16, dtype=torch.float32).reshape(4, 4)
+    got, want = run_gpu((4, 4), "float32", (2, 2), "S^{01}R", (2, 2), "S^0R", x)
+    assert_same(got, want)
+
+
+@pytest.mark.parametrize("case", range(1, 10))
+def test_table3_scaled(case):
+    import json
+    here = os.path.dirname(__file__)
+    c = json.load(open(os.path.join(here, "golden", "table3_cases.json")))["cases"][case - 1]
+    shape = (64, 48, 40)
+    _say(f"table3 case {case} {shape}")
+    for flags in (0, B.RESHARD_SENDER_NAIVE):
+        x = rand_bits(shape, "float16", case)
+        got, want = run_gpu(shape, "float16", tuple(c["send_mesh"]), c["send_spec"], tuple(c["recv_mesh"]),
+                            c["recv_spec"], x, flags=flags)
+        assert_same(got, want)
+
+
+@pytest.mark.parametrize("case", _fuzz(60, 5))
+def test_fuzz_small(case):
+    shape, dt, sm, ss, dm, ds, flags = case
+    _say(f"fuzz {case}")
+    got, want = run_gpu(shape, dt, sm, ss, dm, ds, rand_bits(shape, dt, 3), flags=flags)
+    assert_same(got, want)
+
+
+def _mid_cases(n, seed):
+    rng = random.Random(seed)
+    out = []
+    while len(out) < n:
+        ndim = rng.randint(2, 4)
+        shape = tuple(rng.choice([1, 3, 17, 64, 97, 130, 256]) for _ in range(ndim))
+        if int(np.prod(shape)) > 3_000_000:
+            continue
+        sm = tuple(rng.randint(1, 4) for _ in range(2))
+        dm = tuple(rng.randint(1, 4) for _ in range(2))
+        out.append((shape, rng.choice(["uint8", "float16", "float32", "float64"]), sm,
+                    fmt_spec(random_dims(rng, ndim, 2)), dm, fmt_spec(random_dims(rng, ndim, 2))))
+    return out
+
+
+@pytest.mark.parametrize("case", _mid_cases(24, 77))
+def test_fuzz_multi_tile_ragged(case):
+    # sizes spanning many chunks with ragged tails and misaligned phases
+    shape, dt, sm, ss, dm, ds = case
+    _say(f"mid {case}")
+    for kw in ({}, {"chunk_bytes": 1000, "block_threads": 64}, {"chunk_bytes": 70000, "block_threads": 1024}):
+        got, want = run_gpu(shape, dt, sm, ss, dm, ds, rand_bits(shape, dt, 4), **kw)
+        assert_same(got, want)
+
+
+def test_no_xcd_remap_flag():
+    w = WORKLOADS[5]
+    shape = (2, 64, 384)
+    x = rand_bits(shape, w.dtype, 9)
+    got, want = run_gpu(shape, w.dtype, w.src_mesh, w.src_spec, w.dst_mesh, w.dst_spec, x,
+                        flags=B.RESHARD_NO_XCD_REMAP)
+    assert_same(got, want)
+
+
+def test_special_bit_patterns():
+    bits = np.array([0x7E01, 0xFE02, 0x8000, 0x7C00, 0xFC00, 0x0001, 0x7FFF, 0xFFFF] * 64, dtype=np.uint16)
+    x = torch.from_numpy(bits.view(np.float16).reshape(16, 32).copy())
+    got, want = run_gpu((16, 32), "float16", (2,), "S^0R", (2, 2), "RS^1", x)
+    assert_same(got, want)
+
+
+def test_empty_shards_null_pointers_and_empty_tensor():
+    x = rand_bits((3, 40), "float32", 1)
+    got, want = run_gpu((3, 40), "float32", (4,), "S^0R", (2,), "RS^0", x)
+    assert_same(got, want)
+    p = B.reshard_plan((0, 4), "float32", (2,), "S^0R", (2,), "RS^0")
+    B.reshard_execute(p, [None, None], [None, None])
+    torch.cuda.synchronize()
+
+
+def test_misaligned_pointer_rejected():
+    p = B.reshard_plan((8, 64), "float16", (2,), "S^0R", (2,), "RS^0")
+    assert B.reshard_plan_alignment(p) == 16
+    a = torch.zeros(1024, dtype=torch.uint8, device="cuda")
+    src = [a.data_ptr() + 2, a.data_ptr() + 512]
+    with pytest.raises(B.ReshardError) as e:
+        B.reshard_execute(p, src, [a.data_ptr(), a.data_ptr() + 512])
+    assert e.value.status == B.RESHARD_EINVAL
+
+
+def test_plan_reuse_on_streams():
+    shape = (64, 256)
+    x = rand_bits(shape, "float32", 2)
+    xs = as_numpy_bits(x)
+    src = oracle.shard(xs, (2, 2), "S^0S^1")
+    want = oracle.reshard(src, shape, (2, 2), "S^0S^1", (4,), "RS^0")
+    p = B.reshard_plan(shape, "float32", (2, 2), "S^0S^1", (4,), "RS^0")
+    sd = [torch.from_numpy(a.copy()).cuda() for a in src]
+    s1, s2 = torch.cuda.Stream(), torch.cuda.Stream()
+    for s in (s1, s2, None, s1):
+        dd = [torch.empty(w.shape, dtype=torch.int32, device="cuda") for w in want]
+        B.reshard_execute(p, sd, dd, stream=s)
+        torch.cuda.synchronize()
+        for d, w in zip(dd, want):
+            assert np.array_equal(d.cpu().numpy().view(np.uint32), w)
+
+
+@pytest.mark.parametrize("wid", sorted(WORKLOADS))
+def test_workload_full_size(wid):
+    """Full-size workload, bench launch configuration, every output compared."""
+    w = WORKLOADS[wid]
+    _say(f"workload {wid} {w.name} {w.shape}")
+    x = make_workload_tensor(w, seed=0)
+    xb = as_numpy_bits(x)
+    es = xb.dtype.itemsize
+    src = oracle.shard(xb, w.src_mesh, w.src_spec)
+    del xb
+    want = oracle.reshard(src, w.shape, w.src_mesh, w.src_spec, w.dst_mesh, w.dst_spec)
+    p = B.reshard_plan(w.shape, w.dtype, w.src_mesh, w.src_spec, w.dst_mesh, w.dst_spec)
+    sd = [torch.from_numpy(a).cuda() for a in src]
+    del src
+    dd = B.empty_shards(p, 1)
+    for d in dd:
+        d.view(torch.uint8 if es == 1 else torch.int16 if es == 2 else torch.int32).fill_(-1 if es > 1 else 255)
+    B.reshard_execute(p, sd, dd)
+    torch.cuda.synchronize()
+    for k, (d, wnt) in enumerate(zip(dd, want)):
+        g = as_numpy_bits(d)
+        assert g.shape == wnt.shape
+        assert np.array_equal(g, wnt), f"workload {wid} destination {k} differs"
+    _say(f"workload {wid} ok")
