@@ -117,7 +117,9 @@ def main():
     # source mesh by the library itself (a reshard from one buffer).
     x = make_workload_tensor(w, seed=args.seed, device="cuda")
     rep = "".join("R" for _ in w.shape)
-    scatter = B.reshard_plan(w.shape, w.dtype, (1,), rep, w.src_mesh, w.src_spec)
+    # (setup and check launches use 1024-thread workgroups so kernel traces
+    # tell them apart from the timed launches)
+    scatter = B.reshard_plan(w.shape, w.dtype, (1,), rep, w.src_mesh, w.src_spec, block_threads=1024)
     src = B.empty_shards(scatter, 1)
     B.reshard_execute(scatter, [x], src)
 
@@ -146,7 +148,7 @@ def main():
     ms_per_step = ms_total / args.steps
 
     # Round-trip check through the library: dst -> one buffer must equal x.
-    back_plan = B.reshard_plan(w.shape, w.dtype, w.dst_mesh, w.dst_spec, (1,), rep)
+    back_plan = B.reshard_plan(w.shape, w.dtype, w.dst_mesh, w.dst_spec, (1,), rep, block_threads=1024)
     back = B.empty_shards(back_plan, 1)
     B.reshard_execute(back_plan, dst, back)
     torch.cuda.synchronize()

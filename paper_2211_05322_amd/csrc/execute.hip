@@ -46,9 +46,29 @@ struct KArgs {
     void *ptr[NPTR];
 };
 
+// Build knobs (defaults are the measured best): vectors in flight per lane,
+// and the non-temporal hint on source loads / receiver stores.
 #ifndef RS_UNROLL
 #define RS_UNROLL 4
 #endif
+#ifndef RS_NT_LOAD
+#define RS_NT_LOAD 1
+#endif
+#ifndef RS_NT_STORE
+#define RS_NT_STORE 1
+#endif
+
+template <typename V>
+__device__ __forceinline__ V load_vec(const V *p) {
+    if constexpr (RS_NT_LOAD) return __builtin_nontemporal_load(p);
+    else return *p;
+}
+
+template <typename V>
+__device__ __forceinline__ void store_vec(V *p, V x) {
+    if constexpr (RS_NT_STORE) __builtin_nontemporal_store(x, p);
+    else *p = x;
+}
 
 template <int W, int L, int NPTR>
 __device__ __forceinline__ void run_chunk(const Desc &d, const KArgs<NPTR> &a) {
@@ -66,7 +86,7 @@ __device__ __forceinline__ void run_chunk(const Desc &d, const KArgs<NPTR> &a) {
             const uint32_t vi = v + u * nthr;
             if (vi < end) {
                 const Offsets o = piece_offsets<L>(d, vi, W);
-                x[u] = __builtin_nontemporal_load(reinterpret_cast<const V *>(src + o.src));
+                x[u] = load_vec(reinterpret_cast<const V *>(src + o.src));
                 doff[u] = o.dst;
             }
         }
@@ -75,7 +95,7 @@ __device__ __forceinline__ void run_chunk(const Desc &d, const KArgs<NPTR> &a) {
 #pragma unroll
             for (int u = 0; u < U; ++u) {
                 const uint32_t vi = v + u * nthr;
-                if (vi < end) __builtin_nontemporal_store(x[u], reinterpret_cast<V *>(dst + doff[u]));
+                if (vi < end) store_vec(reinterpret_cast<V *>(dst + doff[u]), x[u]);
             }
         }
     }
