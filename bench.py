@@ -91,6 +91,10 @@ def main():
     ap.add_argument("--flags", type=int, default=0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-budget", type=float, default=10.0, help="seconds of oracle timing")
+    ap.add_argument("--no-context", action="store_true", help="skip the device copy/fill ceiling")
+    ap.add_argument("--calib-copy-mib", type=int, default=0,
+                    help="after timing, run a plain device copy of this many MiB 3 times "
+                         "(a known-size kernel for hardware counter calibration)")
     args = ap.parse_args()
 
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
@@ -157,6 +161,40 @@ def main():
 
     nbytes = st["bytes_read"] + st["bytes_written"]
     gbs = nbytes / (ms_per_step * 1e-3) / 1e9
+
+    context = None
+    if not args.no_context:
+        # The same box's plain device copy (read N + write N) and fill (write
+        # N) at the reshard's total traffic, timed the same way: context for
+        # the roofline fraction, not part of the metric.
+        half = (nbytes // 2) & ~4095
+        a = torch.empty(half, dtype=torch.uint8, device="cuda")
+        c = torch.empty_like(a)
+
+        def _rate(fn, moved):
+            fn()
+            torch.cuda.synchronize()
+            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            e0.record(stream)
+            for _ in range(10):
+                fn()
+            e1.record(stream)
+            torch.cuda.synchronize()
+            return moved / (e0.elapsed_time(e1) / 10 * 1e-3) / 1e9
+
+        context = {"device_copy_GBps": round(_rate(lambda: c.copy_(a), 2 * half), 1),
+                   "device_fill_GBps": round(_rate(lambda: c.fill_(7), half), 1),
+                   "bytes_each": half}
+        del a, c
+    if args.calib_copy_mib:
+        n = args.calib_copy_mib << 20
+        a = torch.empty(n, dtype=torch.uint8, device="cuda")
+        c = torch.empty_like(a)
+        torch.cuda.synchronize()
+        for _ in range(3):
+            c.copy_(a)
+        torch.cuda.synchronize()
+        del a, c
     traffic = measured_traffic(w.name)
     out = {
         "metric": METRIC,
@@ -182,6 +220,7 @@ def main():
             "bound": "hbm", "achieved": round(gbs, 2), "peak": HBM_PEAK_GBS, "unit": "GB/s",
             "frac": round(gbs / HBM_PEAK_GBS, 4), "traffic": traffic,
         },
+        "context": context,
         "plan_us": round(plan_us, 1),
         "host_us_per_execute": round(host_us, 2),
         "roundtrip_ok": roundtrip_ok,

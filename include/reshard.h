@@ -66,8 +66,11 @@ typedef enum {
 #define RESHARD_SENDER_NAIVE 0x1u  /* lowest-indexed owner sends (Section 3.2, "Naive
                                       algorithm"); default is longest-first greedy
                                       balancing of sent bytes per device (Eq. 4). */
-#define RESHARD_NO_XCD_REMAP 0x2u  /* launch chunks in table order instead of giving each
-                                      XCD a contiguous run of chunks. */
+#define RESHARD_XCD_REMAP 0x2u     /* give each of the 8 XCDs a contiguous run of the chunk
+                                      table (default: chunks start in table order). */
+#define RESHARD_TASK_ORDER 0x4u    /* keep the chunk table task by task (default: ordered by
+                                      destination address -- receiver set, then offset -- so
+                                      workgroups running together fill whole destination rows). */
 
 /* Compiled limits (RESHARD_EUNSUPPORTED beyond them). */
 #define RESHARD_MAX_NDIM 8
@@ -76,10 +79,13 @@ typedef enum {
 
 /* Optional tuning of the lowering; zero fields take the defaults. */
 typedef struct {
-    int64_t chunk_bytes;    /* source bytes per workgroup chunk (default: sized to fill
-                               256 CUs, 4 KiB..256 KiB); rounded to whole vectors */
+    int64_t chunk_bytes;    /* source bytes per workgroup chunk (default: 4..16 KiB, sized
+                               so a large plan has >= 4096 chunks); whole vectors */
     int32_t block_threads;  /* threads per workgroup: 64, 128, 256, 512 or 1024 (default 256) */
-    int32_t reserved[5];    /* must be zero */
+    int32_t max_wgs_per_cu; /* cap on resident workgroups per CU, 2..32, enforced by reserving
+                               LDS per workgroup; 0 = default (12 waves per CU, at least 2
+                               workgroups); -1 = no cap */
+    int32_t reserved[4];    /* must be zero */
 } reshard_tuning_t;
 
 /*
@@ -106,7 +112,8 @@ reshard_status_t reshard_plan(int ndim, const int64_t *shape, reshard_dtype_t dt
                               unsigned flags, reshard_plan_t **out);
 
 /* As reshard_plan, with lowering knobs (NULL = defaults).  EINVAL for a bad
- * block size, a negative chunk size or non-zero reserved fields. */
+ * block size, a negative chunk size, a workgroup cap outside -1, 0, 2..32 or
+ * non-zero reserved fields. */
 reshard_status_t reshard_plan_ex(int ndim, const int64_t *shape, reshard_dtype_t dtype,
                                  int src_mesh_ndim, const int64_t *src_mesh, const char *src_spec,
                                  int dst_mesh_ndim, const int64_t *dst_mesh, const char *dst_spec,

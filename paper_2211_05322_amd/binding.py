@@ -18,7 +18,8 @@ LIB_PATH = os.path.join(PKG, "libreshard.so")
 
 RESHARD_OK, RESHARD_EINVAL, RESHARD_EUNSUPPORTED, RESHARD_ENOMEM, RESHARD_EHIP = range(5)
 RESHARD_SENDER_NAIVE = 0x1
-RESHARD_NO_XCD_REMAP = 0x2
+RESHARD_XCD_REMAP = 0x2
+RESHARD_TASK_ORDER = 0x4
 RESHARD_MAX_BUFFERS = 496
 
 _DTYPES = {"uint8": 0, "int8": 1, "float16": 2, "bfloat16": 3, "float32": 4, "int32": 5,
@@ -36,7 +37,7 @@ class ReshardError(RuntimeError):
 
 class reshard_tuning_t(ctypes.Structure):
     _fields_ = [("chunk_bytes", ctypes.c_int64), ("block_threads", ctypes.c_int32),
-                ("reserved", ctypes.c_int32 * 5)]
+                ("max_wgs_per_cu", ctypes.c_int32), ("reserved", ctypes.c_int32 * 4)]
 
 
 _lib = None
@@ -142,13 +143,14 @@ class Plan:
 
 
 def reshard_plan(shape, dtype, src_mesh, src_spec, dst_mesh, dst_spec, flags=0,
-                 chunk_bytes=0, block_threads=0):
+                 chunk_bytes=0, block_threads=0, max_wgs_per_cu=0):
     lib = load()
     h = ctypes.c_void_p()
     args = [len(shape), _i64(shape), _dtype_code(dtype), len(src_mesh), _i64(src_mesh),
             src_spec.encode(), len(dst_mesh), _i64(dst_mesh), dst_spec.encode(), int(flags)]
-    if chunk_bytes or block_threads:
-        t = reshard_tuning_t(chunk_bytes=int(chunk_bytes), block_threads=int(block_threads))
+    if chunk_bytes or block_threads or max_wgs_per_cu:
+        t = reshard_tuning_t(chunk_bytes=int(chunk_bytes), block_threads=int(block_threads),
+                             max_wgs_per_cu=int(max_wgs_per_cu))
         _check(lib.reshard_plan_ex(*args, ctypes.byref(t), ctypes.byref(h)))
     else:
         _check(lib.reshard_plan(*args, ctypes.byref(h)))

@@ -1,5 +1,6 @@
 // capi.cpp -- C ABI of libreshard.so: planning, queries, host interpreter.
 // reshard_execute and the kernel live in execute.hip.
+#include <algorithm>
 #include <cstring>
 #include <new>
 #include <string>
@@ -71,7 +72,7 @@ reshard_status_t make_plan(int ndim, const int64_t *shape, reshard_dtype_t dtype
         if (!mul_ok(total, shape[i], int64_t(1) << 56, total))
             return fail(RESHARD_EUNSUPPORTED, "tensor larger than 2^56 bytes");
     }
-    if (flags & ~(RESHARD_SENDER_NAIVE | RESHARD_NO_XCD_REMAP))
+    if (flags & ~(RESHARD_SENDER_NAIVE | RESHARD_XCD_REMAP | RESHARD_TASK_ORDER))
         return fail(RESHARD_EINVAL, "unknown flag bits");
     rs::Tuning tn;
     if (tuning) {
@@ -81,8 +82,20 @@ reshard_status_t make_plan(int ndim, const int64_t *shape, reshard_dtype_t dtype
         const int bt = tuning->block_threads;
         if (bt != 0 && bt != 64 && bt != 128 && bt != 256 && bt != 512 && bt != 1024)
             return fail(RESHARD_EINVAL, "tuning.block_threads must be 64, 128, 256, 512 or 1024");
+        const int cap = tuning->max_wgs_per_cu;
+        if (cap != 0 && cap != -1 && (cap < 2 || cap > 32))
+            return fail(RESHARD_EINVAL, "tuning.max_wgs_per_cu must be -1, 0 or 2..32");
         tn.chunk_bytes = tuning->chunk_bytes;
         if (bt) tn.block_threads = bt;
+        tn.max_wgs_per_cu = cap;
+    }
+    if (tn.max_wgs_per_cu == 0) {
+        // default residency: about 12 waves per CU (fewer concurrent write
+        // streams schedule better in HBM), never below 2 workgroups
+        const int waves = tn.block_threads / 64;
+        tn.max_wgs_per_cu = std::max(2, 12 / waves);
+    } else if (tn.max_wgs_per_cu == -1) {
+        tn.max_wgs_per_cu = 0;
     }
     int64_t ns = 0, nd = 0;
     reshard_status_t st = check_mesh("source", smn, sm, ns);
@@ -226,13 +239,13 @@ reshard_status_t reshard_debug_execute_host(const reshard_plan_t *plan, void *co
     for (const rs::Desc &d : p->descs) {
         const uint32_t w = 1u << rs::kind_log2w(d.kind);
         const uint32_t levels = rs::kind_levels(d.kind);
-        const char *src = static_cast<const char *>(src_ptrs[d.src_buf]);
+        const char *src = static_cast<const char *>(src_ptrs[d.src_buf]) + d.src_base;
         for (uint32_t v = d.v0; v < d.v1; ++v) {
-            const rs::Offsets o = levels == 1   ? rs::piece_offsets<1>(d, v, w)
-                                  : levels == 2 ? rs::piece_offsets<2>(d, v, w)
-                                                : rs::piece_offsets<3>(d, v, w);
+            const rs::Rel o = levels == 1   ? rs::chunk_offsets<1>(d, v, w)
+                              : levels == 2 ? rs::chunk_offsets<2>(d, v, w)
+                                            : rs::chunk_offsets<3>(d, v, w);
             for (uint32_t r = 0; r < d.nfan; ++r) {
-                char *dst = static_cast<char *>(dst_ptrs[p->fan[d.fan_off + r]]);
+                char *dst = static_cast<char *>(dst_ptrs[p->fan[d.fan_off + r]]) + d.dst_base;
                 std::memcpy(dst + o.dst, src + o.src, w);
             }
         }

@@ -8,6 +8,14 @@
 // every receiver gets the same bytes at the same local offset (replicas of a
 // destination slice share one local layout).
 //
+// Addressing: a descriptor carries the 64-bit byte offsets of its chunk's
+// first vector (src_base / dst_base).  Offsets inside a piece grow with the
+// vector index (dense C-order strides), and the planner keeps every chunk's
+// span below 2^32 bytes on both sides, so the offset of any vector relative
+// to the chunk's first one is computed exactly in 32-bit modular arithmetic
+// from strides taken modulo 2^32.  The kernel thus forms every address as a
+// workgroup-uniform 64-bit base plus a 32-bit per-lane offset.
+//
 // Index arithmetic uses division by invariant integers through a multiply and
 // shift (Granlund & Montgomery, "Division by invariant integers using
 // multiplication", PLDI 1994, the round-up method for N = 32): for a divisor
@@ -43,10 +51,12 @@ constexpr uint32_t kind_log2w(uint32_t kind) { return kind & 0xFu; }
 constexpr uint32_t kind_levels(uint32_t kind) { return kind >> 4; }
 
 struct alignas(16) Desc {
-    uint64_t src_off;    // byte offset of the piece origin in the sender buffer
-    uint64_t dst_off;    // byte offset of the piece origin in every receiver buffer
-    int64_t ss[3];       // sender byte strides of outer levels 1..3 (1 = innermost)
-    int64_t ds[3];       // receiver byte strides of outer levels 1..3
+    uint64_t src_base;   // byte offset of the chunk's first vector in the sender buffer
+    uint64_t dst_base;   // byte offset of the chunk's first vector in every receiver buffer
+    uint32_t ss[3];      // sender byte strides of outer levels 1..3 (1 = innermost), mod 2^32
+    uint32_t ds[3];      // receiver byte strides of outer levels 1..3, mod 2^32
+    uint32_t src_rel0;   // piece-relative sender offset of vector v0, mod 2^32
+    uint32_t dst_rel0;   // piece-relative receiver offset of vector v0, mod 2^32
     uint32_t v0, v1;     // this chunk: vectors [v0, v1) of the piece
     uint32_t vpr;        // vectors per run
     uint32_t n1, n2;     // extents of outer levels 1 and 2 (level 3 is bounded by v1)
@@ -57,39 +67,39 @@ struct alignas(16) Desc {
     uint16_t nfan;       // number of receivers
     uint32_t fan_off;    // receivers: fan[fan_off .. fan_off + nfan) index the dst table
 };
-static_assert(sizeof(Desc) == 112, "descriptor layout is shared by host and device");
+static_assert(sizeof(Desc) == 96, "descriptor layout is shared by host and device");
 
-// Byte offsets (sender, receiver) of vector v of a descriptor's piece.
-struct Offsets {
-    uint64_t src;
-    uint64_t dst;
+// Offsets (sender, receiver) of vector v relative to the chunk's first vector.
+struct Rel {
+    uint32_t src;
+    uint32_t dst;
 };
 
 template <int LEVELS>
-constexpr Offsets piece_offsets(const Desc &d, uint32_t v, uint32_t vbytes) {
+constexpr Rel chunk_offsets(const Desc &d, uint32_t v, uint32_t vbytes) {
     const uint32_t row = fastdiv(v, d.mul_vpr, d.sh_vpr);
     const uint32_t col = v - row * d.vpr;
-    uint64_t s = uint64_t(col) * vbytes;
-    uint64_t t = s;
+    uint32_t s = col * vbytes;
+    uint32_t t = s;
     if (LEVELS == 1) {
-        s += uint64_t(row) * uint64_t(d.ss[0]);
-        t += uint64_t(row) * uint64_t(d.ds[0]);
+        s += row * d.ss[0];
+        t += row * d.ds[0];
     } else {
         const uint32_t r2 = fastdiv(row, d.mul_n1, d.sh_n1);
         const uint32_t r1 = row - r2 * d.n1;
-        s += uint64_t(r1) * uint64_t(d.ss[0]);
-        t += uint64_t(r1) * uint64_t(d.ds[0]);
+        s += r1 * d.ss[0];
+        t += r1 * d.ds[0];
         if (LEVELS == 2) {
-            s += uint64_t(r2) * uint64_t(d.ss[1]);
-            t += uint64_t(r2) * uint64_t(d.ds[1]);
+            s += r2 * d.ss[1];
+            t += r2 * d.ds[1];
         } else {
             const uint32_t r3 = fastdiv(r2, d.mul_n2, d.sh_n2);
             const uint32_t q2 = r2 - r3 * d.n2;
-            s += uint64_t(q2) * uint64_t(d.ss[1]) + uint64_t(r3) * uint64_t(d.ss[2]);
-            t += uint64_t(q2) * uint64_t(d.ds[1]) + uint64_t(r3) * uint64_t(d.ds[2]);
+            s += q2 * d.ss[1] + r3 * d.ss[2];
+            t += q2 * d.ds[1] + r3 * d.ds[2];
         }
     }
-    return Offsets{s + d.src_off, t + d.dst_off};
+    return Rel{s - d.src_rel0, t - d.dst_rel0};
 }
 
 }  // namespace rs

@@ -24,6 +24,7 @@ namespace rs {
 reshard_status_t fail(reshard_status_t st, const std::string &msg);
 
 #define RS_CONST __attribute__((address_space(4)))
+#define RS_GLOBAL __attribute__((address_space(1)))
 
 typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
 typedef unsigned int u32x2 __attribute__((ext_vector_type(2)));
@@ -49,86 +50,189 @@ struct KArgs {
 // Build knobs (defaults are the measured best): vectors in flight per lane,
 // and the non-temporal hint on source loads / receiver stores.
 #ifndef RS_UNROLL
-#define RS_UNROLL 4
+#define RS_UNROLL 2
 #endif
 #ifndef RS_NT_LOAD
-#define RS_NT_LOAD 1
+#define RS_NT_LOAD 0
 #endif
 #ifndef RS_NT_STORE
 #define RS_NT_STORE 1
 #endif
 
 template <typename V>
-__device__ __forceinline__ V load_vec(const V *p) {
+__device__ __forceinline__ V load_vec(const RS_GLOBAL V *p) {
     if constexpr (RS_NT_LOAD) return __builtin_nontemporal_load(p);
     else return *p;
 }
 
 template <typename V>
-__device__ __forceinline__ void store_vec(V *p, V x) {
+__device__ __forceinline__ void store_vec(RS_GLOBAL V *p, V x) {
     if constexpr (RS_NT_STORE) __builtin_nontemporal_store(x, p);
     else *p = x;
 }
 
-template <int W, int L, int NPTR>
-__device__ __forceinline__ void run_chunk(const Desc &d, const KArgs<NPTR> &a) {
+#ifndef RS_PIPELINE
+#define RS_PIPELINE 1
+#endif
+#ifndef RS_DRAIN
+#define RS_DRAIN 0  // 1: wait for a batch's stores before the next batch's loads
+#endif
+#ifndef RS_STORE_ORDER
+#define RS_STORE_ORDER 0  // 0: receiver-major stores, 1: vector-major stores
+#endif
+
+// Load one batch of U vectors per lane (vectors v, v+nthr, ...).  FULL: the
+// whole batch is inside the chunk (a workgroup-uniform fact), so no lane
+// needs a bounds check and the loop carries no divergent branches.
+template <int W, int L, int U, bool FULL>
+__device__ __forceinline__ void load_batch(const Desc &d, const RS_GLOBAL char *src, uint32_t v, uint32_t nthr,
+                                           uint32_t end, typename Vec<W>::T (&x)[U], uint32_t (&doff)[U]) {
     typedef typename Vec<W>::T V;
-    constexpr int U = RS_UNROLL;
-    const char *src = static_cast<const char *>(a.ptr[d.src_buf]);
-    const RS_CONST int32_t *fan = (const RS_CONST int32_t *)(a.fan + d.fan_off);
-    const uint32_t nthr = blockDim.x;
-    const uint32_t end = d.v1;
-    for (uint32_t v = d.v0 + threadIdx.x; v < end; v += U * nthr) {
-        V x[U];
-        uint64_t doff[U];
 #pragma unroll
-        for (int u = 0; u < U; ++u) {
-            const uint32_t vi = v + u * nthr;
-            if (vi < end) {
-                const Offsets o = piece_offsets<L>(d, vi, W);
-                x[u] = load_vec(reinterpret_cast<const V *>(src + o.src));
-                doff[u] = o.dst;
-            }
-        }
-        for (uint32_t r = 0; r < d.nfan; ++r) {
-            char *dst = static_cast<char *>(a.ptr[a.nsrc + uint32_t(fan[r])]);
-#pragma unroll
-            for (int u = 0; u < U; ++u) {
-                const uint32_t vi = v + u * nthr;
-                if (vi < end) store_vec(reinterpret_cast<V *>(dst + doff[u]), x[u]);
-            }
+    for (int u = 0; u < U; ++u) {
+        const uint32_t vi = v + u * nthr;
+        if (FULL || vi < end) {
+            const Rel o = chunk_offsets<L>(d, vi, W);
+            x[u] = load_vec((const RS_GLOBAL V *)(src + o.src));
+            doff[u] = o.dst;
         }
     }
 }
 
+// Store one batch to every receiver.  RF > 0: the fan-out is a compile-time
+// constant (straight-line stores, so the wait counts stay exact); RF == 0:
+// runtime receiver count.
+template <int W, int U, int RF, bool FULL, int NPTR>
+__device__ __forceinline__ void store_batch(const Desc &d, const RS_CONST KArgs<NPTR> *a, const RS_CONST int32_t *fan,
+                                            uint32_t v, uint32_t nthr, uint32_t end,
+                                            const typename Vec<W>::T (&x)[U], const uint32_t (&doff)[U]) {
+    typedef typename Vec<W>::T V;
+    const uint32_t nr = RF > 0 ? uint32_t(RF) : d.nfan;
+    if (RS_STORE_ORDER == 1 && RF > 0) {
+#pragma unroll
+        for (int u = 0; u < U; ++u) {
+            const uint32_t vi = v + u * nthr;
+#pragma unroll
+            for (uint32_t r = 0; r < nr; ++r) {
+                RS_GLOBAL char *dst = (RS_GLOBAL char *)a->ptr[a->nsrc + uint32_t(fan[r])] + d.dst_base;
+                if (FULL || vi < end) store_vec((RS_GLOBAL V *)(dst + doff[u]), x[u]);
+            }
+        }
+    } else {
+#pragma unroll
+        for (uint32_t r = 0; r < nr; ++r) {
+            RS_GLOBAL char *dst = (RS_GLOBAL char *)a->ptr[a->nsrc + uint32_t(fan[r])] + d.dst_base;
+#pragma unroll
+            for (int u = 0; u < U; ++u) {
+                const uint32_t vi = v + u * nthr;
+                if (FULL || vi < end) store_vec((RS_GLOBAL V *)(dst + doff[u]), x[u]);
+            }
+        }
+    }
+    if (RS_DRAIN) asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+}
+
+template <int W, int L, int RF, int NPTR>
+__device__ __forceinline__ void run_chunk(const Desc &d, const RS_CONST KArgs<NPTR> *a) {
+    typedef typename Vec<W>::T V;
+    constexpr int U = RS_UNROLL;
+    const RS_GLOBAL char *src = (const RS_GLOBAL char *)a->ptr[d.src_buf] + d.src_base;
+    const RS_CONST int32_t *fan = (const RS_CONST int32_t *)(a->fan + d.fan_off);
+    const uint32_t nthr = blockDim.x;
+    const uint32_t end = d.v1;
+    const uint32_t step = U * nthr;
+    const uint32_t tid = threadIdx.x;
+    uint32_t base = d.v0;  // workgroup-uniform batch start
+    if (RS_PIPELINE) {
+        // two register sets: the next batch's loads are in flight while the
+        // current batch is stored
+        V x[U], y[U];
+        uint32_t dx[U], dy[U];
+        if (base + step <= end) {
+            load_batch<W, L, U, true>(d, src, base + tid, nthr, end, x, dx);
+            for (;;) {
+                if (base + 2 * step > end) {
+                    store_batch<W, U, RF, true>(d, a, fan, base + tid, nthr, end, x, dx);
+                    base += step;
+                    break;
+                }
+                load_batch<W, L, U, true>(d, src, base + step + tid, nthr, end, y, dy);
+                store_batch<W, U, RF, true>(d, a, fan, base + tid, nthr, end, x, dx);
+                base += step;
+                if (base + 2 * step > end) {
+                    store_batch<W, U, RF, true>(d, a, fan, base + tid, nthr, end, y, dy);
+                    base += step;
+                    break;
+                }
+                load_batch<W, L, U, true>(d, src, base + step + tid, nthr, end, x, dx);
+                store_batch<W, U, RF, true>(d, a, fan, base + tid, nthr, end, y, dy);
+                base += step;
+            }
+        }
+    } else {
+        for (; base + step <= end; base += step) {
+            V x[U];
+            uint32_t doff[U];
+            load_batch<W, L, U, true>(d, src, base + tid, nthr, end, x, doff);
+            store_batch<W, U, RF, true>(d, a, fan, base + tid, nthr, end, x, doff);
+        }
+    }
+    if (base < end) {  // ragged tail: per-lane bounds checks
+        V x[U];
+        uint32_t doff[U];
+        load_batch<W, L, U, false>(d, src, base + tid, nthr, end, x, doff);
+        store_batch<W, U, RF, false>(d, a, fan, base + tid, nthr, end, x, doff);
+    }
+}
+
+// 16-byte path: fan-outs 1..8 get their own straight-line store sequence.
+template <int L, int NPTR>
+__device__ __forceinline__ void run_wide(const Desc &d, const RS_CONST KArgs<NPTR> *a) {
+    switch (d.nfan) {
+        case 1: run_chunk<16, L, 1>(d, a); break;
+        case 2: run_chunk<16, L, 2>(d, a); break;
+        case 3: run_chunk<16, L, 3>(d, a); break;
+        case 4: run_chunk<16, L, 4>(d, a); break;
+        case 5: run_chunk<16, L, 5>(d, a); break;
+        case 6: run_chunk<16, L, 6>(d, a); break;
+        case 7: run_chunk<16, L, 7>(d, a); break;
+        case 8: run_chunk<16, L, 8>(d, a); break;
+        default: run_chunk<16, L, 0>(d, a); break;
+    }
+}
+
 template <int NPTR>
-__global__ __launch_bounds__(1024) void reshard_kernel(KArgs<NPTR> a) {
+__global__ __launch_bounds__(1024) void reshard_kernel(KArgs<NPTR> args) {
+    // The argument block is read in place through the kernarg segment pointer
+    // (constant address space): pointer-table lookups with a uniform index
+    // become scalar loads and nothing is copied to private memory.
+    const RS_CONST KArgs<NPTR> *a = (const RS_CONST KArgs<NPTR> *)__builtin_amdgcn_kernarg_segment_ptr();
     const uint32_t b = blockIdx.x;
-    const uint32_t idx = a.per_xcd ? (b & 7u) * a.per_xcd + (b >> 3) : b;
-    if (idx >= a.ndesc) return;
+    const uint32_t idx = a->per_xcd ? (b & 7u) * a->per_xcd + (b >> 3) : b;
+    if (idx >= a->ndesc) return;
     // uniform load through the constant address space -> scalar registers
-    const RS_CONST u32x4 *q = (const RS_CONST u32x4 *)(a.descs + idx);
+    const RS_CONST u32x4 *q = (const RS_CONST u32x4 *)(a->descs + idx);
     u32x4 raw[sizeof(Desc) / 16];
 #pragma unroll
     for (int i = 0; i < int(sizeof(Desc) / 16); ++i) raw[i] = q[i];
     Desc d;
     __builtin_memcpy(&d, raw, sizeof(Desc));
     switch (d.kind) {
-        case make_kind(4, 1): run_chunk<16, 1>(d, a); break;
-        case make_kind(4, 2): run_chunk<16, 2>(d, a); break;
-        case make_kind(4, 3): run_chunk<16, 3>(d, a); break;
-        case make_kind(3, 1): run_chunk<8, 1>(d, a); break;
-        case make_kind(3, 2): run_chunk<8, 2>(d, a); break;
-        case make_kind(3, 3): run_chunk<8, 3>(d, a); break;
-        case make_kind(2, 1): run_chunk<4, 1>(d, a); break;
-        case make_kind(2, 2): run_chunk<4, 2>(d, a); break;
-        case make_kind(2, 3): run_chunk<4, 3>(d, a); break;
-        case make_kind(1, 1): run_chunk<2, 1>(d, a); break;
-        case make_kind(1, 2): run_chunk<2, 2>(d, a); break;
-        case make_kind(1, 3): run_chunk<2, 3>(d, a); break;
-        case make_kind(0, 1): run_chunk<1, 1>(d, a); break;
-        case make_kind(0, 2): run_chunk<1, 2>(d, a); break;
-        case make_kind(0, 3): run_chunk<1, 3>(d, a); break;
+        case make_kind(4, 1): run_wide<1>(d, a); break;
+        case make_kind(4, 2): run_wide<2>(d, a); break;
+        case make_kind(4, 3): run_wide<3>(d, a); break;
+        case make_kind(3, 1): run_chunk<8, 1, 0>(d, a); break;
+        case make_kind(3, 2): run_chunk<8, 2, 0>(d, a); break;
+        case make_kind(3, 3): run_chunk<8, 3, 0>(d, a); break;
+        case make_kind(2, 1): run_chunk<4, 1, 0>(d, a); break;
+        case make_kind(2, 2): run_chunk<4, 2, 0>(d, a); break;
+        case make_kind(2, 3): run_chunk<4, 3, 0>(d, a); break;
+        case make_kind(1, 1): run_chunk<2, 1, 0>(d, a); break;
+        case make_kind(1, 2): run_chunk<2, 2, 0>(d, a); break;
+        case make_kind(1, 3): run_chunk<2, 3, 0>(d, a); break;
+        case make_kind(0, 1): run_chunk<1, 1, 0>(d, a); break;
+        case make_kind(0, 2): run_chunk<1, 2, 0>(d, a); break;
+        case make_kind(0, 3): run_chunk<1, 3, 0>(d, a); break;
         default: break;
     }
 }
@@ -182,11 +286,23 @@ reshard_status_t launch(const Plan &p, const Desc *descs, const int32_t *fan, vo
     for (int64_t k = 0; k < p.dst.ndev; ++k) a.ptr[p.src.ndev + k] = dst_ptrs[k];
     uint32_t grid = a.ndesc;
     a.per_xcd = 0;
-    if (!(p.flags & RESHARD_NO_XCD_REMAP)) {
+    if (p.flags & RESHARD_XCD_REMAP) {
         a.per_xcd = (a.ndesc + 7u) / 8u;
         grid = a.per_xcd * 8u;
     }
-    hipLaunchKernelGGL(reshard_kernel<NPTR>, dim3(grid), dim3(uint32_t(p.tuning.block_threads)), 0, stream, a);
+    // An LDS reservation (unused by the kernel) caps resident workgroups per
+    // CU: the CU holds 160 KiB of LDS.
+    const uint32_t lds = p.tuning.max_wgs_per_cu ? (160u * 1024u / uint32_t(p.tuning.max_wgs_per_cu)) & ~1023u : 0u;
+    if (lds > 64u * 1024u) {
+        static bool raised = false;  // per kernel instantiation
+        if (!raised) {
+            const hipError_t ea = hipFuncSetAttribute(reinterpret_cast<const void *>(&reshard_kernel<NPTR>),
+                                                      hipFuncAttributeMaxDynamicSharedMemorySize, int(lds));
+            if (ea != hipSuccess) return hip_fail("raising the kernel's LDS limit", ea);
+            raised = true;
+        }
+    }
+    hipLaunchKernelGGL(reshard_kernel<NPTR>, dim3(grid), dim3(uint32_t(p.tuning.block_threads)), lds, stream, a);
     const hipError_t e = hipGetLastError();
     if (e != hipSuccess) return hip_fail("kernel launch", e);
     return RESHARD_OK;

@@ -213,19 +213,35 @@ int32_t pick_width(uint64_t so, uint64_t dso, int64_t run, const std::vector<Lev
 constexpr uint64_t kMaxPieceVectors = (uint64_t(1) << 31) - 1;
 constexpr uint64_t kMaxDescs = uint64_t(1) << 24;  // 1.75 GiB of descriptors
 
+// 64-bit byte offsets (sender, receiver) of vector v of a piece.
+std::pair<uint64_t, uint64_t> piece_off64(const Piece &pc, uint64_t vpr, uint64_t v) {
+    uint64_t row = v / vpr;
+    const uint64_t col = v - row * vpr;
+    uint64_t s = pc.src_off + col * uint64_t(pc.w), t = pc.dst_off + col * uint64_t(pc.w);
+    const int nl = int(pc.outer.size());
+    for (int i = nl - 1; i >= 0; --i) {
+        const uint64_t n = uint64_t(pc.outer[i].n);
+        const uint64_t idx = i == 0 ? row : row % n;
+        s += idx * uint64_t(pc.outer[i].ss);
+        t += idx * uint64_t(pc.outer[i].ds);
+        row = i == 0 ? 0 : row / n;
+    }
+    return {s, t};
+}
+
+constexpr uint64_t kMaxChunkSpan = uint64_t(1) << 32;
+
 // Emit chunks of a piece whose outer list has at most 3 levels and fewer
-// than 2^31 vectors.
+// than 2^31 vectors.  Every chunk spans less than 2^32 bytes on both sides.
 void emit(Plan &p, const Piece &pc, int32_t src_buf, int64_t fan_off, int64_t nfan, int64_t chunk_bytes) {
     Desc d{};
-    d.src_off = pc.src_off;
-    d.dst_off = pc.dst_off;
     const int nl = int(pc.outer.size());
     const int levels = std::max(1, nl);
     // outer[] is outermost first; Desc level 1 is the innermost outer level
     for (int i = 0; i < nl; ++i) {
         const Level &l = pc.outer[nl - 1 - i];
-        d.ss[i] = l.ss;
-        d.ds[i] = l.ds;
+        d.ss[i] = uint32_t(uint64_t(l.ss));
+        d.ds[i] = uint32_t(uint64_t(l.ds));
     }
     const uint64_t vpr = uint64_t(pc.run / pc.w);
     uint64_t rows = 1;
@@ -252,10 +268,28 @@ void emit(Plan &p, const Piece &pc, int32_t src_buf, int64_t fan_off, int64_t nf
         p.too_many = true;
         return;
     }
-    for (uint64_t v0 = 0; v0 < total; v0 += cv) {
+    for (uint64_t v0 = 0; v0 < total;) {
+        uint64_t v1 = std::min(total, v0 + cv);
+        const auto first = piece_off64(pc, vpr, v0);
+        for (;;) {  // shrink until the chunk spans < 2^32 bytes on both sides
+            const auto last = piece_off64(pc, vpr, v1 - 1);
+            if (last.first + uint64_t(pc.w) - first.first < kMaxChunkSpan &&
+                last.second + uint64_t(pc.w) - first.second < kMaxChunkSpan)
+                break;
+            v1 = v0 + (v1 - v0) / 2;
+        }
+        if (p.descs.size() >= kMaxDescs) {
+            p.too_many = true;
+            return;
+        }
         d.v0 = uint32_t(v0);
-        d.v1 = uint32_t(std::min(total, v0 + cv));
+        d.v1 = uint32_t(v1);
+        d.src_base = first.first;
+        d.dst_base = first.second;
+        d.src_rel0 = uint32_t(first.first - pc.src_off);
+        d.dst_rel0 = uint32_t(first.second - pc.dst_off);
         p.descs.push_back(d);
+        v0 = v1;
     }
     p.align = std::max<int64_t>(p.align, pc.w);
 }
@@ -320,9 +354,9 @@ void split_emit(Plan &p, Piece pc, int32_t src_buf, int64_t fan_off, int64_t nfa
 }
 
 int64_t auto_chunk_bytes(int64_t bytes_read) {
-    // Enough chunks to fill 256 CUs several times over, 4 KiB .. 64 KiB each.
+    // Enough chunks to fill 256 CUs many times over, 4 KiB .. 16 KiB each.
     int64_t c = 4096;
-    while (c < 65536 && bytes_read / (2 * c) >= 4096) c *= 2;
+    while (c < 16384 && bytes_read / (2 * c) >= 4096) c *= 2;
     return c;
 }
 
@@ -408,6 +442,17 @@ void lower(Plan &p) {
             parts.push_back(pc);
         }
         for (const auto &pc : parts) split_emit(p, pc, t.sender, fan_off, nfan, chunk);
+    }
+    if (!(p.flags & 0x4u)) {
+        // destination-major chunk order: receiver set, then the byte offset
+        // of the chunk's first vector in the receivers' buffers
+        std::vector<std::pair<std::pair<uint32_t, uint64_t>, size_t>> key(p.descs.size());
+        for (size_t i = 0; i < p.descs.size(); ++i) key[i] = {{p.descs[i].fan_off, p.descs[i].dst_base}, i};
+        std::stable_sort(key.begin(), key.end(),
+                         [](const auto &a, const auto &b) { return a.first < b.first; });
+        std::vector<Desc> sorted(p.descs.size());
+        for (size_t i = 0; i < key.size(); ++i) sorted[i] = p.descs[key[i].second];
+        p.descs.swap(sorted);
     }
     p.bytes_written = 0;
     p.dst_local_numel.assign(p.dst.ndev, 0);

@@ -45,6 +45,7 @@ struct UnitTask {
 struct Tuning {
     int64_t chunk_bytes = 0;   // 0: automatic
     int32_t block_threads = 256;
+    int32_t max_wgs_per_cu = 0;  // resolved cap (0: none)
 };
 
 struct Plan {

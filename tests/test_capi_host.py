@@ -108,7 +108,8 @@ def _fuzz(n, seed, max_len=12):
         dm = tuple(rng.randint(1, 4) for _ in range(rng.randint(1, 3)))
         out.append((shape, rng.choice(["uint8", "float16", "float32", "float64"]), sm,
                     fmt_spec(random_dims(rng, ndim, len(sm))), dm, fmt_spec(random_dims(rng, ndim, len(dm))),
-                    rng.choice([0, 0, B.RESHARD_SENDER_NAIVE])))
+                    rng.choice([0, 0, B.RESHARD_SENDER_NAIVE, B.RESHARD_TASK_ORDER,
+                                B.RESHARD_XCD_REMAP | B.RESHARD_SENDER_NAIVE])))
     return out
 
 
@@ -238,7 +239,10 @@ def test_query_errors():
     assert lib.reshard_plan_local_shape(p.handle, 0, 5, out) == B.RESHARD_EINVAL
     assert lib.reshard_plan_unit_task(p.handle, 99, out, out, None, None, 0, None, None, 0, None) == B.RESHARD_EINVAL
     with pytest.raises(B.ReshardError):
-        B.reshard_plan(( 4, 4), "float16", (2,), "RR", (2,), "RR", block_threads=100)
+        B.reshard_plan((4, 4), "float16", (2,), "RR", (2,), "RR", block_threads=100)
+    for cap in (1, 33, -2):
+        with pytest.raises(B.ReshardError):
+            B.reshard_plan((4, 4), "float16", (2,), "RR", (2,), "RR", max_wgs_per_cu=cap)
 
 
 def test_execute_rejects_null_buffer_on_host_interpreter():

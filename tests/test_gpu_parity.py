@@ -150,17 +150,21 @@ def test_fuzz_multi_tile_ragged(case):
     # sizes spanning many chunks with ragged tails and misaligned phases
     shape, dt, sm, ss, dm, ds = case
     _say(f"mid {case}")
-    for kw in ({}, {"chunk_bytes": 1000, "block_threads": 64}, {"chunk_bytes": 70000, "block_threads": 1024}):
+    for kw in ({}, {"chunk_bytes": 1000, "block_threads": 64, "max_wgs_per_cu": 2},
+               {"chunk_bytes": 70000, "block_threads": 1024, "max_wgs_per_cu": -1}):
         got, want = run_gpu(shape, dt, sm, ss, dm, ds, rand_bits(shape, dt, 4), **kw)
         assert_same(got, want)
 
 
-def test_no_xcd_remap_flag():
+@pytest.mark.parametrize("flags", [B.RESHARD_XCD_REMAP, B.RESHARD_TASK_ORDER,
+                                   B.RESHARD_XCD_REMAP | B.RESHARD_TASK_ORDER | B.RESHARD_SENDER_NAIVE])
+@pytest.mark.parametrize("cap", [-1, 2, 32])
+def test_launch_order_flags_and_residency_caps(flags, cap):
     w = WORKLOADS[5]
     shape = (2, 64, 384)
     x = rand_bits(shape, w.dtype, 9)
     got, want = run_gpu(shape, w.dtype, w.src_mesh, w.src_spec, w.dst_mesh, w.dst_spec, x,
-                        flags=B.RESHARD_NO_XCD_REMAP)
+                        flags=flags, chunk_bytes=4096, max_wgs_per_cu=cap)
     assert_same(got, want)
 
 
