@@ -71,6 +71,12 @@ typedef enum {
 #define RESHARD_TASK_ORDER 0x4u    /* keep the chunk table task by task (default: ordered by
                                       destination address -- receiver set, then offset -- so
                                       workgroups running together fill whole destination rows). */
+#define RESHARD_NO_REALIGN 0x8u    /* rows whose source and destination 16-byte phases differ
+                                      are copied with narrow vectors instead of being
+                                      realigned into 16-byte destination slots. */
+#define RESHARD_LDS_STAGING 0x10u  /* such rows are realigned by staging source words in LDS
+                                      (default: two overlapping aligned loads per slot,
+                                      funnel-shifted in registers). */
 
 /* Compiled limits (RESHARD_EUNSUPPORTED beyond them). */
 #define RESHARD_MAX_NDIM 8
@@ -165,6 +171,15 @@ reshard_status_t reshard_plan_stats(const reshard_plan_t *plan, int64_t *bytes_r
 /* Required byte alignment of every buffer pointer passed to reshard_execute
  * (1..16), or 0 for a NULL plan. */
 int64_t reshard_plan_alignment(const reshard_plan_t *plan);
+
+/* LDS bytes per workgroup the plan's realignment chunks stage rows through
+ * (0 unless RESHARD_LDS_STAGING is set and some rows need realigning), or -1
+ * for a NULL plan. */
+int64_t reshard_plan_lds_bytes(const reshard_plan_t *plan);
+
+/* Number of workgroup chunks that realign rows (source and destination in
+ * different 16-byte phases), or -1 for a NULL plan. */
+int64_t reshard_plan_realign_chunks(const reshard_plan_t *plan);
 
 /*
  * Unit task `index` (0 <= index < n_unit_tasks), in lexicographic order of the

@@ -20,6 +20,8 @@ RESHARD_OK, RESHARD_EINVAL, RESHARD_EUNSUPPORTED, RESHARD_ENOMEM, RESHARD_EHIP =
 RESHARD_SENDER_NAIVE = 0x1
 RESHARD_XCD_REMAP = 0x2
 RESHARD_TASK_ORDER = 0x4
+RESHARD_NO_REALIGN = 0x8
+RESHARD_LDS_STAGING = 0x10
 RESHARD_MAX_BUFFERS = 496
 
 _DTYPES = {"uint8": 0, "int8": 1, "float16": 2, "bfloat16": 3, "float32": 4, "int32": 5,
@@ -70,6 +72,10 @@ def load(path=None):
     lib.reshard_plan_stats.restype = ctypes.c_int
     lib.reshard_plan_alignment.argtypes = [ctypes.c_void_p]
     lib.reshard_plan_alignment.restype = ctypes.c_int64
+    lib.reshard_plan_lds_bytes.argtypes = [ctypes.c_void_p]
+    lib.reshard_plan_lds_bytes.restype = ctypes.c_int64
+    lib.reshard_plan_realign_chunks.argtypes = [ctypes.c_void_p]
+    lib.reshard_plan_realign_chunks.restype = ctypes.c_int64
     lib.reshard_plan_unit_task.argtypes = [ctypes.c_void_p, ctypes.c_int64, _I64P, _I64P, _I64P,
                                            _I64P, ctypes.c_int64, _I64P, _I64P, ctypes.c_int64, _I64P]
     lib.reshard_plan_unit_task.restype = ctypes.c_int
@@ -203,6 +209,14 @@ def reshard_plan_stats(plan):
 
 def reshard_plan_alignment(plan):
     return int(load().reshard_plan_alignment(plan.handle))
+
+
+def reshard_plan_lds_bytes(plan):
+    return int(load().reshard_plan_lds_bytes(plan.handle))
+
+
+def reshard_plan_realign_chunks(plan):
+    return int(load().reshard_plan_realign_chunks(plan.handle))
 
 
 def reshard_plan_unit_task(plan, index):

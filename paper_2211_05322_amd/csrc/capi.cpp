@@ -4,6 +4,7 @@
 #include <cstring>
 #include <new>
 #include <string>
+#include <vector>
 
 #include "../../include/reshard.h"
 #include "planner.hpp"
@@ -72,7 +73,7 @@ reshard_status_t make_plan(int ndim, const int64_t *shape, reshard_dtype_t dtype
         if (!mul_ok(total, shape[i], int64_t(1) << 56, total))
             return fail(RESHARD_EUNSUPPORTED, "tensor larger than 2^56 bytes");
     }
-    if (flags & ~(RESHARD_SENDER_NAIVE | RESHARD_XCD_REMAP | RESHARD_TASK_ORDER))
+    if (flags & ~(RESHARD_SENDER_NAIVE | RESHARD_XCD_REMAP | RESHARD_TASK_ORDER | RESHARD_NO_REALIGN | RESHARD_LDS_STAGING))
         return fail(RESHARD_EINVAL, "unknown flag bits");
     rs::Tuning tn;
     if (tuning) {
@@ -201,6 +202,17 @@ int64_t reshard_plan_alignment(const reshard_plan_t *plan) {
     return p ? p->align : 0;
 }
 
+int64_t reshard_plan_lds_bytes(const reshard_plan_t *plan) {
+    const rs::Plan *p = as_plan(plan);
+    if (!p) return -1;
+    return (p->flags & RESHARD_LDS_STAGING) ? int64_t(p->lds_bytes) : 0;
+}
+
+int64_t reshard_plan_realign_chunks(const reshard_plan_t *plan) {
+    const rs::Plan *p = as_plan(plan);
+    return p ? int64_t(p->descs.size() - p->n_direct) : -1;
+}
+
 reshard_status_t reshard_plan_unit_task(const reshard_plan_t *plan, int64_t index, int64_t *lo, int64_t *hi,
                                         int64_t *chosen_sender, int64_t *senders, int64_t senders_cap,
                                         int64_t *n_senders, int64_t *receivers, int64_t receivers_cap,
@@ -236,10 +248,107 @@ reshard_status_t reshard_debug_execute_host(const reshard_plan_t *plan, void *co
     for (int64_t k = 0; k < p->dst.ndev; ++k)
         if (p->dst_local_numel[k] > 0 && !dst_ptrs[k])
             return fail(RESHARD_EINVAL, "destination buffer " + std::to_string(k) + " is NULL but its shard is not empty");
+    std::vector<uint8_t> lds;
     for (const rs::Desc &d : p->descs) {
         const uint32_t w = 1u << rs::kind_log2w(d.kind);
         const uint32_t levels = rs::kind_levels(d.kind);
         const char *src = static_cast<const char *>(src_ptrs[d.src_buf]) + d.src_base;
+        if (rs::kind_realign(d.kind) && !(p->flags & RESHARD_LDS_STAGING)) {
+            // The kernel's shifted-load realignment, same arithmetic: every
+            // loaded word must hold a byte of its row.
+            const uint32_t m = d.vpr, run = d.run, sb = uint32_t(d.src_base), db = uint32_t(d.dst_base);
+            const uint32_t n = (d.v1 - d.v0) * m;
+            auto load_word = [&](const rs::Rel &o, uint32_t sph, int32_t j, uint32_t out[4]) -> bool {
+                const int32_t off = int32_t(o.src - sph + 16u * uint32_t(j));
+                const int64_t rel = int64_t(off) - int64_t(o.src);  // row-relative word start
+                if (rel + 16 <= 0 || rel >= int64_t(run)) return false;
+                if (((sb + uint32_t(off)) & 15u) != 0) return false;
+                uint8_t b[16] = {0};
+                for (int64_t t = 0; t < 16; ++t)
+                    if (rel + t >= 0 && rel + t < int64_t(run)) b[t] = uint8_t(src[int64_t(off) + t]);
+                std::memcpy(out, b, 16);
+                return true;
+            };
+            for (uint32_t i = 0; i < n; ++i) {
+                const uint32_t br = rs::fastdiv(i, d.mul_vpr, d.sh_vpr), k = i - br * m;
+                const rs::Rel o = levels == 1 ? rs::row_offsets<1>(d, d.v0 + br)
+                                  : levels == 2 ? rs::row_offsets<2>(d, d.v0 + br) : rs::row_offsets<3>(d, d.v0 + br);
+                const uint32_t sph = (sb + o.src) & 15u, tph = (db + o.dst) & 15u;
+                const int32_t start = int32_t(16u * k) - int32_t(tph);
+                const int32_t lo = std::max(start, 0), hi = std::min(start + 16, int32_t(run));
+                if (lo >= hi) continue;
+                const int32_t pos = int32_t(sph) + start;
+                const int32_t j0 = pos >> 4;
+                uint32_t w[8] = {0};
+                if (j0 >= 0 && !load_word(o, sph, j0, w)) return fail(RESHARD_EINVAL, "internal: shifted load outside its row");
+                if (16 * (j0 + 1) < int32_t(sph + run) && !load_word(o, sph, j0 + 1, w + 4))
+                    return fail(RESHARD_EINVAL, "internal: shifted load outside its row");
+                const uint32_t sh = uint32_t(pos) & 15u, t4 = sh >> 2, b = sh & 3u;
+                uint32_t v[4];
+                for (uint32_t t = 0; t < 4; ++t) v[t] = rs::align_byte(w[t4 + t + 1], w[t4 + t], b);
+                uint8_t bytes[16];
+                std::memcpy(bytes, v, 16);
+                for (uint32_t r = 0; r < d.nfan; ++r) {
+                    char *dst = static_cast<char *>(dst_ptrs[p->fan[d.fan_off + r]]) + d.dst_base + o.dst;
+                    for (int32_t c = lo; c < hi; ++c) dst[c] = char(bytes[c - start]);
+                }
+            }
+            continue;
+        }
+        if (rs::kind_realign(d.kind)) {
+            // Same staging layout, slot arithmetic and dword funnel shifts as
+            // the kernel's LDS path, with every staging access bounds-checked.
+            const uint32_t m = d.vpr, run = d.run, sb = uint32_t(d.src_base), db = uint32_t(d.dst_base);
+            lds.assign(rs::realign_lds_bytes(d.batch, m), 0);
+            auto row_off = [&](uint32_t row) {
+                return levels == 1 ? rs::row_offsets<1>(d, row)
+                       : levels == 2 ? rs::row_offsets<2>(d, row) : rs::row_offsets<3>(d, row);
+            };
+            for (uint32_t r0 = d.v0; r0 < d.v1; r0 += d.batch) {
+                const uint32_t nb = std::min(d.batch, d.v1 - r0);
+                std::fill(lds.begin(), lds.end(), 0);
+                for (uint32_t i = 0; i < nb * m; ++i) {
+                    const uint32_t br = rs::fastdiv(i, d.mul_vpr, d.sh_vpr), j = i - br * m;
+                    const rs::Rel o = row_off(r0 + br);
+                    const uint32_t ph = (sb + o.src) & 15u;
+                    if (16u * j >= ph + run) continue;
+                    const uint32_t at = rs::kRealignFront + 16u * i;
+                    if (at + 16u > lds.size()) return fail(RESHARD_EINVAL, "internal: staging write out of range");
+                    // the kernel's signed 32-bit word offset; copy only the
+                    // row's bytes of the aligned source word
+                    const int32_t off = int32_t(o.src + 16u * j - ph);
+                    const int64_t wbeg = int64_t(o.src) - ph + 16 * int64_t(j);
+                    if (int64_t(off) != wbeg) return fail(RESHARD_EINVAL, "internal: staging word offset wraps");
+                    if (((sb + uint32_t(off)) & 15u) != 0) return fail(RESHARD_EINVAL, "internal: staging word misaligned");
+                    for (int64_t b = 0; b < 16; ++b) {
+                        const int64_t pos = wbeg + b - int64_t(o.src);  // row-relative
+                        if (pos >= 0 && pos < int64_t(run)) lds[at + b] = uint8_t(src[wbeg + b]);
+                    }
+                }
+                for (uint32_t i = 0; i < nb * m; ++i) {
+                    const uint32_t br = rs::fastdiv(i, d.mul_vpr, d.sh_vpr), k = i - br * m;
+                    const rs::Rel o = row_off(r0 + br);
+                    const uint32_t sph = (sb + o.src) & 15u, tph = (db + o.dst) & 15u;
+                    const int32_t start = int32_t(16u * k) - int32_t(tph);
+                    const int32_t lo = std::max(start, 0), hi = std::min(start + 16, int32_t(run));
+                    if (lo >= hi) continue;
+                    const uint32_t q = rs::kRealignFront + br * m * 16u + uint32_t(int32_t(sph) + start);
+                    const uint32_t q4 = q >> 2, sh = q & 3u;
+                    if (4u * (q4 + 5u) > lds.size()) return fail(RESHARD_EINVAL, "internal: staging read out of range");
+                    uint32_t wd[5];
+                    std::memcpy(wd, lds.data() + 4u * q4, sizeof(wd));
+                    uint32_t v[4];
+                    for (int t = 0; t < 4; ++t) v[t] = rs::align_byte(wd[t + 1], wd[t], sh);
+                    uint8_t bytes[16];
+                    std::memcpy(bytes, v, 16);
+                    for (uint32_t r = 0; r < d.nfan; ++r) {
+                        char *dst = static_cast<char *>(dst_ptrs[p->fan[d.fan_off + r]]) + d.dst_base + o.dst;
+                        for (int32_t b = lo; b < hi; ++b) dst[b] = char(bytes[b - start]);
+                    }
+                }
+            }
+            continue;
+        }
         for (uint32_t v = d.v0; v < d.v1; ++v) {
             const rs::Rel o = levels == 1   ? rs::chunk_offsets<1>(d, v, w)
                               : levels == 2 ? rs::chunk_offsets<2>(d, v, w)

@@ -45,10 +45,30 @@ constexpr uint32_t fastdiv(uint32_t n, uint32_t mul, uint32_t shift) {
     return uint32_t((t + n) >> shift);
 }
 
-// Kernel variant: log2 of the vector width and the number of outer levels.
+// Kernel variant: log2 of the vector width, the number of outer levels, and
+// whether the chunk takes the LDS realignment path (source and destination
+// rows in different 16-byte phases).
+constexpr uint32_t kRealign = 0x80u;
 constexpr uint32_t make_kind(uint32_t log2w, uint32_t levels) { return log2w | (levels << 4); }
 constexpr uint32_t kind_log2w(uint32_t kind) { return kind & 0xFu; }
-constexpr uint32_t kind_levels(uint32_t kind) { return kind >> 4; }
+constexpr uint32_t kind_levels(uint32_t kind) { return (kind >> 4) & 0x7u; }
+constexpr bool kind_realign(uint32_t kind) { return (kind & kRealign) != 0; }
+
+// LDS realignment path.  A workgroup stages `batch` rows of a chunk at a
+// time: row i of the batch occupies words [i*m, (i+1)*m) of the staging area,
+// which starts kRealignFront bytes into LDS; word j of a row holds the
+// source's 16-byte aligned word j counted from the one holding the row's
+// first byte.  m = words per staged row = (run + 30) / 16 bounds both the
+// source words and the 16-byte destination slots a row of `run` bytes can
+// touch.  kRealignBack bytes after the last row keep the 5-dword reads of
+// the last slot inside the allocation.
+constexpr uint32_t kRealignFront = 16;
+constexpr uint32_t kRealignBack = 32;
+constexpr uint32_t kRealignStageBytes = 16384;  // staged row bytes per pass, at most
+constexpr uint32_t realign_words(uint32_t run) { return (run + 30u) / 16u; }
+constexpr uint32_t realign_lds_bytes(uint32_t batch, uint32_t m) {
+    return kRealignFront + batch * m * 16u + kRealignBack;
+}
 
 struct alignas(16) Desc {
     uint64_t src_base;   // byte offset of the chunk's first vector in the sender buffer
@@ -61,13 +81,16 @@ struct alignas(16) Desc {
     uint32_t vpr;        // vectors per run
     uint32_t n1, n2;     // extents of outer levels 1 and 2 (level 3 is bounded by v1)
     uint32_t mul_vpr, mul_n1, mul_n2;  // fast-division multipliers
+    uint32_t run;        // realignment path: bytes per row (v0, v1, vpr then count rows / words)
+    uint32_t batch;      // realignment path: rows staged in LDS per pass
     uint8_t sh_vpr, sh_n1, sh_n2;      // fast-division shifts
-    uint8_t kind;        // make_kind(log2 W, levels), levels in 1..3
+    uint8_t kind;        // make_kind(log2 W, levels) [| kRealign], levels in 1..3
     uint16_t src_buf;    // sender: index into the source pointer table
     uint16_t nfan;       // number of receivers
     uint32_t fan_off;    // receivers: fan[fan_off .. fan_off + nfan) index the dst table
+    uint32_t pad[3];
 };
-static_assert(sizeof(Desc) == 96, "descriptor layout is shared by host and device");
+static_assert(sizeof(Desc) == 112, "descriptor layout is shared by host and device");
 
 // Offsets (sender, receiver) of vector v relative to the chunk's first vector.
 struct Rel {
@@ -75,12 +98,12 @@ struct Rel {
     uint32_t dst;
 };
 
+// Offsets of the start of row `row` of the piece relative to the chunk's
+// first vector (mod 2^32).
 template <int LEVELS>
-constexpr Rel chunk_offsets(const Desc &d, uint32_t v, uint32_t vbytes) {
-    const uint32_t row = fastdiv(v, d.mul_vpr, d.sh_vpr);
-    const uint32_t col = v - row * d.vpr;
-    uint32_t s = col * vbytes;
-    uint32_t t = s;
+constexpr Rel row_offsets(const Desc &d, uint32_t row) {
+    uint32_t s = 0;
+    uint32_t t = 0;
     if (LEVELS == 1) {
         s += row * d.ss[0];
         t += row * d.ds[0];
@@ -100,6 +123,19 @@ constexpr Rel chunk_offsets(const Desc &d, uint32_t v, uint32_t vbytes) {
         }
     }
     return Rel{s - d.src_rel0, t - d.dst_rel0};
+}
+
+template <int LEVELS>
+constexpr Rel chunk_offsets(const Desc &d, uint32_t v, uint32_t vbytes) {
+    const uint32_t row = fastdiv(v, d.mul_vpr, d.sh_vpr);
+    const uint32_t col = v - row * d.vpr;
+    const Rel r = row_offsets<LEVELS>(d, row);
+    return Rel{r.src + col * vbytes, r.dst + col * vbytes};
+}
+
+// v_alignbyte semantics: bytes [sh, sh+4) of the 8-byte value hi:lo.
+constexpr uint32_t align_byte(uint32_t hi, uint32_t lo, uint32_t sh) {
+    return uint32_t(((uint64_t(hi) << 32) | lo) >> (8u * sh));
 }
 
 }  // namespace rs

@@ -185,6 +185,114 @@ __device__ __forceinline__ void run_chunk(const Desc &d, const RS_CONST KArgs<NP
     }
 }
 
+// Write bytes [lo, hi) (0 <= lo < hi <= 16) of the 16-byte value v to
+// slot[lo, hi), where slot is 16-byte aligned: naturally aligned 8/4/2/1-byte
+// pieces, at most six stores.
+__device__ __forceinline__ void store_partial(RS_GLOBAL unsigned char *slot, u32x4 v, uint32_t lo, uint32_t hi) {
+    const uint64_t q0 = (uint64_t(v.y) << 32) | v.x, q1 = (uint64_t(v.w) << 32) | v.z;
+#pragma nounroll
+    while (lo < hi) {
+        const uint64_t q = lo < 8 ? q0 : q1;
+        const uint32_t sh = 8u * (lo & 7u);
+        if ((lo & 7u) == 0 && lo + 8 <= hi) {
+            *(RS_GLOBAL uint64_t *)(slot + lo) = q;
+            lo += 8;
+        } else if ((lo & 3u) == 0 && lo + 4 <= hi) {
+            *(RS_GLOBAL uint32_t *)(slot + lo) = uint32_t(q >> sh);
+            lo += 4;
+        } else if ((lo & 1u) == 0 && lo + 2 <= hi) {
+            *(RS_GLOBAL uint16_t *)(slot + lo) = uint16_t(q >> sh);
+            lo += 2;
+        } else {
+            slot[lo] = (unsigned char)(q >> sh);
+            lo += 1;
+        }
+    }
+}
+
+// LDS realignment path for rows whose source and destination 16-byte phases
+// differ.  Per pass over `batch` rows: (1) every source word a row touches is
+// loaded once, 16-byte aligned and coalesced, into the row's staging slot in
+// LDS; (2) each lane builds one 16-byte destination slot from five staged
+// dwords (v_alignbyte funnel shift by the row's phase difference) and stores
+// it, aligned, to every receiver; slots cut by the row's ends are written
+// byte by byte.  A source word is loaded only if it holds a byte of the row,
+// so it never leaves the row's 4 KiB page.
+template <int L, int NPTR>
+__device__ __forceinline__ void run_realign(const Desc &d, const RS_CONST KArgs<NPTR> *a) {
+    extern __shared__ __attribute__((aligned(16))) unsigned char rs_lds[];
+    const uint32_t m = d.vpr, run = d.run;
+    const uint32_t sb = uint32_t(d.src_base), db = uint32_t(d.dst_base);
+    const RS_GLOBAL char *src = (const RS_GLOBAL char *)a->ptr[d.src_buf] + d.src_base;
+    const RS_CONST int32_t *fan = (const RS_CONST int32_t *)(a->fan + d.fan_off);
+    const uint32_t nthr = blockDim.x, tid = threadIdx.x;
+    for (uint32_t r0 = d.v0; r0 < d.v1; r0 += d.batch) {
+        const uint32_t n = (d.v1 - r0 < d.batch ? d.v1 - r0 : d.batch) * m;
+        // stage: up to 4 words per lane per round, all loads issued first
+        for (uint32_t i0 = 0; i0 < n; i0 += 4u * nthr) {
+            u32x4 w[4];
+            bool ok[4];
+#pragma unroll
+            for (int u = 0; u < 4; ++u) {
+                const uint32_t i = i0 + tid + uint32_t(u) * nthr;
+                ok[u] = false;
+                if (i < n) {
+                    const uint32_t br = fastdiv(i, d.mul_vpr, d.sh_vpr);
+                    const uint32_t j = i - br * m;
+                    const Rel o = row_offsets<L>(d, r0 + br);
+                    const uint32_t ph = (sb + o.src) & 15u;
+                    if (16u * j < ph + run) {
+                        // the word holding the row's first byte can start up to
+                        // 15 bytes before the chunk base: a signed offset (chunk
+                        // spans stay below 2^31 on this path)
+                        const int32_t off = int32_t(o.src + 16u * j - ph);
+                        w[u] = load_vec((const RS_GLOBAL u32x4 *)(src + off));
+                        ok[u] = true;
+                    }
+                }
+            }
+#pragma unroll
+            for (int u = 0; u < 4; ++u) {
+                const uint32_t i = i0 + tid + uint32_t(u) * nthr;
+                if (ok[u]) *reinterpret_cast<u32x4 *>(rs_lds + kRealignFront + 16u * i) = w[u];
+            }
+        }
+        __syncthreads();
+        for (uint32_t i = tid; i < n; i += nthr) {
+            const uint32_t br = fastdiv(i, d.mul_vpr, d.sh_vpr);
+            const uint32_t k = i - br * m;
+            const Rel o = row_offsets<L>(d, r0 + br);
+            const uint32_t sph = (sb + o.src) & 15u, tph = (db + o.dst) & 15u;
+            const int32_t start = int32_t(16u * k) - int32_t(tph);  // row-relative slot start
+            const int32_t lo = start > 0 ? start : 0;
+            const int32_t hi = start + 16 < int32_t(run) ? start + 16 : int32_t(run);
+            if (lo >= hi) continue;
+            const uint32_t q = kRealignFront + br * m * 16u + uint32_t(int32_t(sph) + start);
+            const uint32_t *w = reinterpret_cast<const uint32_t *>(rs_lds) + (q >> 2);
+            const uint32_t sh = q & 3u;
+            const uint32_t w0 = w[0], w1 = w[1], w2 = w[2], w3 = w[3], w4 = w[4];
+            u32x4 v;
+            v.x = __builtin_amdgcn_alignbyte(w1, w0, sh);
+            v.y = __builtin_amdgcn_alignbyte(w2, w1, sh);
+            v.z = __builtin_amdgcn_alignbyte(w3, w2, sh);
+            v.w = __builtin_amdgcn_alignbyte(w4, w3, sh);
+            if (lo == start && hi == start + 16) {
+                for (uint32_t r = 0; r < d.nfan; ++r) {
+                    RS_GLOBAL char *dst = (RS_GLOBAL char *)a->ptr[a->nsrc + uint32_t(fan[r])] + d.dst_base;
+                    store_vec((RS_GLOBAL u32x4 *)(dst + (o.dst + uint32_t(start))), v);
+                }
+            } else {
+                for (uint32_t r = 0; r < d.nfan; ++r) {
+                    RS_GLOBAL unsigned char *slot =
+                        (RS_GLOBAL unsigned char *)a->ptr[a->nsrc + uint32_t(fan[r])] + d.dst_base + o.dst + start;
+                    store_partial(slot, v, uint32_t(lo - start), uint32_t(hi - start));
+                }
+            }
+        }
+        __syncthreads();
+    }
+}
+
 // 16-byte path: fan-outs 1..8 get their own straight-line store sequence.
 template <int L, int NPTR>
 __device__ __forceinline__ void run_wide(const Desc &d, const RS_CONST KArgs<NPTR> *a) {
@@ -237,6 +345,115 @@ __global__ __launch_bounds__(1024) void reshard_kernel(KArgs<NPTR> args) {
     }
 }
 
+// Bytes [s, s+16) of the 32-byte value lo:hi (s in 0..15), as four dwords.
+__device__ __forceinline__ u32x4 funnel32(u32x4 lo, u32x4 hi, uint32_t s) {
+    const uint32_t t = s >> 2, b = s & 3u;
+    const uint32_t d0 = lo.x, d1 = lo.y, d2 = lo.z, d3 = lo.w, d4 = hi.x, d5 = hi.y, d6 = hi.z, d7 = hi.w;
+    const uint32_t e0 = t == 0 ? d0 : t == 1 ? d1 : t == 2 ? d2 : d3;
+    const uint32_t e1 = t == 0 ? d1 : t == 1 ? d2 : t == 2 ? d3 : d4;
+    const uint32_t e2 = t == 0 ? d2 : t == 1 ? d3 : t == 2 ? d4 : d5;
+    const uint32_t e3 = t == 0 ? d3 : t == 1 ? d4 : t == 2 ? d5 : d6;
+    const uint32_t e4 = t == 0 ? d4 : t == 1 ? d5 : t == 2 ? d6 : d7;
+    u32x4 v;
+    v.x = __builtin_amdgcn_alignbyte(e1, e0, b);
+    v.y = __builtin_amdgcn_alignbyte(e2, e1, b);
+    v.z = __builtin_amdgcn_alignbyte(e3, e2, b);
+    v.w = __builtin_amdgcn_alignbyte(e4, e3, b);
+    return v;
+}
+
+// Realignment without staging: each lane builds a 16-byte destination slot
+// from the two aligned source words that cover it, loaded directly (the
+// neighbouring lane's overlapping load is served by the cache), funnel-shifted
+// in registers.  Same descriptors as the staging path: slot (row, k) for k <
+// m.  Words holding no byte of the row are not loaded.
+template <int L, int NPTR>
+__device__ __forceinline__ void run_shift(const Desc &d, const RS_CONST KArgs<NPTR> *a) {
+    constexpr int U = 2;
+    const uint32_t m = d.vpr, run = d.run;
+    const uint32_t sb = uint32_t(d.src_base), db = uint32_t(d.dst_base);
+    const RS_GLOBAL char *src = (const RS_GLOBAL char *)a->ptr[d.src_buf] + d.src_base;
+    const RS_CONST int32_t *fan = (const RS_CONST int32_t *)(a->fan + d.fan_off);
+    const uint32_t nthr = blockDim.x, tid = threadIdx.x;
+    const uint32_t n = (d.v1 - d.v0) * m;
+    for (uint32_t i0 = 0; i0 < n; i0 += U * nthr) {
+        u32x4 v[U];
+        int32_t lo[U], hi[U], st[U];
+        uint32_t dof[U];
+#pragma unroll
+        for (int u = 0; u < U; ++u) {
+            const uint32_t i = i0 + tid + uint32_t(u) * nthr;
+            lo[u] = 0;
+            hi[u] = 0;
+            st[u] = 0;
+            dof[u] = 0;
+            if (i < n) {
+                const uint32_t br = fastdiv(i, d.mul_vpr, d.sh_vpr);
+                const uint32_t k = i - br * m;
+                const Rel o = row_offsets<L>(d, d.v0 + br);
+                const uint32_t sph = (sb + o.src) & 15u, tph = (db + o.dst) & 15u;
+                const int32_t start = int32_t(16u * k) - int32_t(tph);
+                lo[u] = start > 0 ? start : 0;
+                hi[u] = start + 16 < int32_t(run) ? start + 16 : int32_t(run);
+                st[u] = start;
+                dof[u] = o.dst;
+                if (lo[u] < hi[u]) {
+                    const int32_t pos = int32_t(sph) + start;  // in the row's word grid, >= -15
+                    const int32_t j0 = pos >> 4;                // arithmetic shift: -1 for the head
+                    u32x4 w0 = {0u, 0u, 0u, 0u}, w1 = {0u, 0u, 0u, 0u};
+                    if (j0 >= 0)
+                        w0 = load_vec((const RS_GLOBAL u32x4 *)(src + int32_t(o.src - sph + 16u * uint32_t(j0))));
+                    if (16 * (j0 + 1) < int32_t(sph + run))
+                        w1 = load_vec((const RS_GLOBAL u32x4 *)(src + int32_t(o.src - sph + 16u * uint32_t(j0 + 1))));
+                    v[u] = funnel32(w0, w1, uint32_t(pos) & 15u);
+                }
+            }
+        }
+        for (uint32_t r = 0; r < d.nfan; ++r) {
+            RS_GLOBAL char *dst = (RS_GLOBAL char *)a->ptr[a->nsrc + uint32_t(fan[r])] + d.dst_base;
+#pragma unroll
+            for (int u = 0; u < U; ++u) {
+                if (lo[u] >= hi[u]) continue;
+                if (lo[u] == st[u] && hi[u] == st[u] + 16) {
+                    store_vec((RS_GLOBAL u32x4 *)(dst + (dof[u] + uint32_t(st[u]))), v[u]);
+                } else {
+                    RS_GLOBAL unsigned char *slot = (RS_GLOBAL unsigned char *)dst + dof[u] + st[u];
+                    store_partial(slot, v[u], uint32_t(lo[u] - st[u]), uint32_t(hi[u] - st[u]));
+                }
+            }
+        }
+    }
+}
+
+// Realignment chunks run in their own kernel so their register use does not
+// bound the direct kernel's occupancy.  STAGE: through LDS, else shifted loads.
+template <int NPTR, bool STAGE>
+__global__ __launch_bounds__(256) void reshard_realign_kernel(KArgs<NPTR> args) {
+    const RS_CONST KArgs<NPTR> *a = (const RS_CONST KArgs<NPTR> *)__builtin_amdgcn_kernarg_segment_ptr();
+    const uint32_t b = blockIdx.x;
+    const uint32_t idx = a->per_xcd ? (b & 7u) * a->per_xcd + (b >> 3) : b;
+    if (idx >= a->ndesc) return;
+    const RS_CONST u32x4 *q = (const RS_CONST u32x4 *)(a->descs + idx);
+    u32x4 raw[sizeof(Desc) / 16];
+#pragma unroll
+    for (int i = 0; i < int(sizeof(Desc) / 16); ++i) raw[i] = q[i];
+    Desc d;
+    __builtin_memcpy(&d, raw, sizeof(Desc));
+    if (STAGE) {
+        switch (kind_levels(d.kind)) {
+            case 1: run_realign<1>(d, a); break;
+            case 2: run_realign<2>(d, a); break;
+            default: run_realign<3>(d, a); break;
+        }
+    } else {
+        switch (kind_levels(d.kind)) {
+            case 1: run_shift<1>(d, a); break;
+            case 2: run_shift<2>(d, a); break;
+            default: run_shift<3>(d, a); break;
+        }
+    }
+}
+
 // ------------------------------------------------------------------ host
 
 namespace {
@@ -273,38 +490,64 @@ reshard_status_t device_table(const Plan &p, int dev, const Desc **descs, const 
     return RESHARD_OK;
 }
 
+template <typename K, typename A>
+reshard_status_t launch_one(K kernel, A a, uint32_t ndesc, bool remap, uint32_t block, uint32_t lds,
+                            hipStream_t stream) {
+    a.ndesc = ndesc;
+    uint32_t grid = ndesc;
+    a.per_xcd = 0;
+    if (remap) {
+        a.per_xcd = (ndesc + 7u) / 8u;
+        grid = a.per_xcd * 8u;
+    }
+    if (lds > 64u * 1024u) {
+        // above the default dynamic-LDS limit; raising it is idempotent
+        const hipError_t ea = hipFuncSetAttribute(reinterpret_cast<const void *>(kernel),
+                                                  hipFuncAttributeMaxDynamicSharedMemorySize, int(lds));
+        if (ea != hipSuccess) return hip_fail("raising the kernel's LDS limit", ea);
+    }
+    hipLaunchKernelGGL(kernel, dim3(grid), dim3(block), lds, stream, a);
+    const hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return hip_fail("kernel launch", e);
+    return RESHARD_OK;
+}
+
 template <int NPTR>
 reshard_status_t launch(const Plan &p, const Desc *descs, const int32_t *fan, void *const *src_ptrs,
                         void *const *dst_ptrs, hipStream_t stream) {
     KArgs<NPTR> a;
     a.descs = descs;
     a.fan = fan;
-    a.ndesc = uint32_t(p.descs.size());
+    a.ndesc = 0;
     a.nsrc = uint32_t(p.src.ndev);
+    a.per_xcd = 0;
     a.pad = 0;
     for (int64_t k = 0; k < p.src.ndev; ++k) a.ptr[k] = src_ptrs[k];
     for (int64_t k = 0; k < p.dst.ndev; ++k) a.ptr[p.src.ndev + k] = dst_ptrs[k];
-    uint32_t grid = a.ndesc;
-    a.per_xcd = 0;
-    if (p.flags & RESHARD_XCD_REMAP) {
-        a.per_xcd = (a.ndesc + 7u) / 8u;
-        grid = a.per_xcd * 8u;
+    const bool remap = (p.flags & RESHARD_XCD_REMAP) != 0;
+    const uint32_t block = uint32_t(p.tuning.block_threads);
+    // An LDS reservation (unused by the direct kernel) caps resident
+    // workgroups per CU: the CU holds 160 KiB of LDS.
+    const uint32_t cap_lds =
+        p.tuning.max_wgs_per_cu ? (160u * 1024u / uint32_t(p.tuning.max_wgs_per_cu)) & ~1023u : 0u;
+    const uint32_t n_direct = uint32_t(p.n_direct), n_realign = uint32_t(p.descs.size() - p.n_direct);
+    if (n_direct) {
+        const reshard_status_t st = launch_one(reshard_kernel<NPTR>, a, n_direct, remap, block, cap_lds, stream);
+        if (st != RESHARD_OK) return st;
     }
-    // An LDS reservation (unused by the kernel) caps resident workgroups per
-    // CU: the CU holds 160 KiB of LDS.
-    const uint32_t lds = p.tuning.max_wgs_per_cu ? (160u * 1024u / uint32_t(p.tuning.max_wgs_per_cu)) & ~1023u : 0u;
-    if (lds > 64u * 1024u) {
-        static bool raised = false;  // per kernel instantiation
-        if (!raised) {
-            const hipError_t ea = hipFuncSetAttribute(reinterpret_cast<const void *>(&reshard_kernel<NPTR>),
-                                                      hipFuncAttributeMaxDynamicSharedMemorySize, int(lds));
-            if (ea != hipSuccess) return hip_fail("raising the kernel's LDS limit", ea);
-            raised = true;
-        }
+    if (n_realign) {
+        a.descs = descs + n_direct;
+        // Realignment kernels hide their load -> shift -> store latency with
+        // resident workgroups: no residency cap (measured: capping at 12
+        // waves per CU halves their throughput).  Staging takes its LDS.
+        const uint32_t need = (p.lds_bytes + 1023u) & ~1023u;
+        const uint32_t rblock = block < 256u ? block : 256u;  // the realignment kernel's bound
+        const reshard_status_t st =
+            (p.flags & RESHARD_LDS_STAGING)
+                ? launch_one(reshard_realign_kernel<NPTR, true>, a, n_realign, remap, rblock, need, stream)
+                : launch_one(reshard_realign_kernel<NPTR, false>, a, n_realign, remap, rblock, 0u, stream);
+        if (st != RESHARD_OK) return st;
     }
-    hipLaunchKernelGGL(reshard_kernel<NPTR>, dim3(grid), dim3(uint32_t(p.tuning.block_threads)), lds, stream, a);
-    const hipError_t e = hipGetLastError();
-    if (e != hipSuccess) return hip_fail("kernel launch", e);
     return RESHARD_OK;
 }
 

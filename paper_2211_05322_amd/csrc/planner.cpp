@@ -190,7 +190,14 @@ struct Piece {
     int64_t run;               // bytes, contiguous on both sides
     std::vector<Level> outer;  // outermost first, at most 3
     int32_t w;                 // vector bytes
+    bool realign = false;      // rows in different 16-byte phases: LDS path
 };
+
+// Rows of at least this many bytes whose source and destination 16-byte
+// phases differ take the LDS realignment path; they are cut into segments of
+// at most kRealignSeg bytes so a pass over a few rows fits the staging area.
+constexpr int64_t kRealignMinRun = 64;
+constexpr int64_t kRealignSeg = 4096;
 
 int64_t pow2_divisor(int64_t x, int64_t cap) {
     int64_t w = cap;
@@ -213,6 +220,10 @@ int32_t pick_width(uint64_t so, uint64_t dso, int64_t run, const std::vector<Lev
 constexpr uint64_t kMaxPieceVectors = (uint64_t(1) << 31) - 1;
 constexpr uint64_t kMaxDescs = uint64_t(1) << 24;  // 1.75 GiB of descriptors
 
+// Index units per row: vectors on the direct path, whole rows on the
+// realignment path.
+uint64_t units_per_row(const Piece &pc) { return pc.realign ? 1 : uint64_t(pc.run / pc.w); }
+
 // 64-bit byte offsets (sender, receiver) of vector v of a piece.
 std::pair<uint64_t, uint64_t> piece_off64(const Piece &pc, uint64_t vpr, uint64_t v) {
     uint64_t row = v / vpr;
@@ -231,9 +242,71 @@ std::pair<uint64_t, uint64_t> piece_off64(const Piece &pc, uint64_t vpr, uint64_
 
 constexpr uint64_t kMaxChunkSpan = uint64_t(1) << 32;
 
+// Realignment path: chunks are ranges of whole rows.
+void emit_realign(Plan &p, const Piece &pc, int32_t src_buf, int64_t fan_off, int64_t nfan, int64_t chunk_bytes) {
+    Desc d{};
+    const int nl = int(pc.outer.size());
+    const int levels = std::max(1, nl);
+    for (int i = 0; i < nl; ++i) {
+        const Level &l = pc.outer[nl - 1 - i];
+        d.ss[i] = uint32_t(uint64_t(l.ss));
+        d.ds[i] = uint32_t(uint64_t(l.ds));
+    }
+    uint64_t rows = 1;
+    for (const auto &l : pc.outer) rows *= uint64_t(l.n);
+    const uint32_t m = realign_words(uint32_t(pc.run));
+    d.run = uint32_t(pc.run);
+    d.vpr = m;
+    d.batch = std::max<uint32_t>(1, kRealignStageBytes / (m * 16u));
+    d.n1 = nl >= 2 ? uint32_t(pc.outer[nl - 1].n) : 1u;
+    d.n2 = nl >= 3 ? uint32_t(pc.outer[nl - 2].n) : 1u;
+    const FastDiv f0 = make_fastdiv(m), f1 = make_fastdiv(d.n1), f2 = make_fastdiv(d.n2);
+    d.mul_vpr = f0.mul; d.sh_vpr = uint8_t(f0.shift);
+    d.mul_n1 = f1.mul;  d.sh_n1 = uint8_t(f1.shift);
+    d.mul_n2 = f2.mul;  d.sh_n2 = uint8_t(f2.shift);
+    d.kind = uint8_t(make_kind(4, uint32_t(levels)) | kRealign);
+    d.src_buf = uint16_t(src_buf);
+    d.nfan = uint16_t(nfan);
+    d.fan_off = uint32_t(fan_off);
+    const uint64_t cr = uint64_t(std::max<int64_t>(1, chunk_bytes / pc.run));  // rows per chunk
+    if (p.descs.size() + (rows + cr - 1) / cr > kMaxDescs) {
+        p.too_many = true;
+        return;
+    }
+    for (uint64_t r0 = 0; r0 < rows;) {
+        uint64_t r1 = std::min(rows, r0 + cr);
+        const auto first = piece_off64(pc, 1, r0);
+        for (;;) {  // spans below 2^31: the kernel forms signed 32-bit word offsets
+            const auto last = piece_off64(pc, 1, r1 - 1);
+            if (last.first + uint64_t(pc.run) - first.first < kMaxChunkSpan / 2 &&
+                last.second + uint64_t(pc.run) - first.second < kMaxChunkSpan / 2)
+                break;
+            r1 = r0 + (r1 - r0) / 2;
+        }
+        if (p.descs.size() >= kMaxDescs) {
+            p.too_many = true;
+            return;
+        }
+        d.v0 = uint32_t(r0);
+        d.v1 = uint32_t(r1);
+        d.src_base = first.first;
+        d.dst_base = first.second;
+        d.src_rel0 = uint32_t(first.first - pc.src_off);
+        d.dst_rel0 = uint32_t(first.second - pc.dst_off);
+        p.descs.push_back(d);
+        r0 = r1;
+    }
+    p.align = std::max<int64_t>(p.align, 16);
+    p.lds_bytes = std::max(p.lds_bytes, realign_lds_bytes(d.batch, m));
+}
+
 // Emit chunks of a piece whose outer list has at most 3 levels and fewer
 // than 2^31 vectors.  Every chunk spans less than 2^32 bytes on both sides.
 void emit(Plan &p, const Piece &pc, int32_t src_buf, int64_t fan_off, int64_t nfan, int64_t chunk_bytes) {
+    if (pc.realign) {
+        emit_realign(p, pc, src_buf, fan_off, nfan, chunk_bytes);
+        return;
+    }
     Desc d{};
     const int nl = int(pc.outer.size());
     const int levels = std::max(1, nl);
@@ -318,7 +391,7 @@ void split_emit(Plan &p, Piece pc, int32_t src_buf, int64_t fan_off, int64_t nfa
     }
     uint64_t rows = 1;
     for (const auto &l : pc.outer) rows *= uint64_t(l.n);
-    const uint64_t vpr = uint64_t(pc.run / pc.w);
+    const uint64_t vpr = units_per_row(pc);
     const uint64_t total = vpr * rows;
     if (total <= kMaxPieceVectors) {
         emit(p, pc, src_buf, fan_off, nfan, chunk_bytes);
@@ -368,6 +441,7 @@ void lower(Plan &p) {
     p.descs.clear();
     p.fan.assign(p.dst.shard_devs.begin(), p.dst.shard_devs.end());
     p.align = 1;
+    p.lds_bytes = 0;
     p.too_many = false;
     p.max_fanout = 0;
     p.bytes_read = 0;
@@ -436,6 +510,14 @@ void lower(Plan &p) {
                 }
                 at += len;
             }
+        } else if (run >= kRealignMinRun && !(p.flags & 0x8u)) {  // 0x8: RESHARD_NO_REALIGN
+            // different 16-byte phases: stage rows through LDS, segments of
+            // at most kRealignSeg bytes
+            for (int64_t at = 0; at < run; at += kRealignSeg) {
+                Piece pc{so + uint64_t(at), dso + uint64_t(at), std::min(kRealignSeg, run - at), g, 16};
+                pc.realign = true;
+                parts.push_back(pc);
+            }
         } else {
             Piece pc{so, dso, run, g, 1};
             pc.w = pick_width(so, dso, run, g);
@@ -454,6 +536,10 @@ void lower(Plan &p) {
         for (size_t i = 0; i < key.size(); ++i) sorted[i] = p.descs[key[i].second];
         p.descs.swap(sorted);
     }
+    // direct chunks first, realignment chunks last (two kernels)
+    std::stable_partition(p.descs.begin(), p.descs.end(), [](const Desc &d) { return !kind_realign(d.kind); });
+    p.n_direct = 0;
+    while (p.n_direct < p.descs.size() && !kind_realign(p.descs[p.n_direct].kind)) ++p.n_direct;
     p.bytes_written = 0;
     p.dst_local_numel.assign(p.dst.ndev, 0);
     p.src_local_numel.assign(p.src.ndev, 0);

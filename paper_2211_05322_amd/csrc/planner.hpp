@@ -61,6 +61,8 @@ struct Plan {
     int64_t bytes_read = 0, bytes_written = 0, max_fanout = 0;
     int64_t align = 1;         // required buffer alignment in bytes
     bool too_many = false;     // lowering stopped: descriptor table over its cap
+    uint32_t lds_bytes = 0;    // LDS the realignment chunks need per workgroup
+    size_t n_direct = 0;       // descs[0, n_direct): direct chunks; the rest: realignment chunks
     std::vector<int64_t> src_local_numel, dst_local_numel;  // per device
 
     // Device copy of [descs | fan], uploaded on the first execute on each HIP

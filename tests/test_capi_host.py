@@ -193,6 +193,44 @@ def test_host_interpreter_misaligned_phase_and_long_runs():
     host_case((3, 4, 3, 4, 3, 8), "uint8", (2, 2, 2), "RS^0RS^1RS^2", (2, 2), "S^0RS^1RRR")
 
 
+# ------------------------------------------------- LDS realignment path
+
+REALIGN_CASES = [
+    # (shape, dtype, src mesh, src spec, dst mesh, dst spec): rows whose source
+    # and destination 16-byte phases differ
+    ((3, 37, 290), "float16", (2, 2), "S^0S^1R", (3,), "RRS^0"),       # odd rows, many phases
+    ((6, 4000), "float16", (3,), "RS^0", (2,), "RS^0"),                 # long rows, 1 dst phase shift
+    ((5, 1000), "uint8", (1,), "RR", (3,), "RS^0"),                     # fan-out 1, byte rows
+    ((4, 96, 70), "float16", (2,), "S^0RR", (2, 2), "RS^0S^1"),         # strides not multiples of 16
+    ((2, 8, 3, 333), "float32", (2, 2), "RS^0RS^1", (3,), "RRRS^0"),    # 3 outer levels
+    ((7, 130), "float64", (2,), "S^0R", (3, 2), "RS^0"),                # fan-out 2 (replicated over axis 1)
+    ((2, 9000), "float16", (1,), "RR", (2,), "RS^0"),                   # rows longer than one segment
+]
+
+
+@pytest.mark.parametrize("case", REALIGN_CASES)
+@pytest.mark.parametrize("chunk", [0, 100, 5000])
+def test_host_realign_path(case, chunk):
+    shape, dt, sm, ss, dm, ds = case
+    p = plan_of(shape, dt, sm, ss, dm, ds, chunk_bytes=chunk)
+    assert B.reshard_plan_realign_chunks(p) > 0, "case should take the realignment path"
+    assert B.reshard_plan_lds_bytes(p) == 0
+    host_case(shape, dt, sm, ss, dm, ds, chunk_bytes=chunk)
+    q = plan_of(shape, dt, sm, ss, dm, ds, flags=B.RESHARD_NO_REALIGN)
+    assert B.reshard_plan_realign_chunks(q) == 0
+    host_case(shape, dt, sm, ss, dm, ds, flags=B.RESHARD_NO_REALIGN)
+    r = plan_of(shape, dt, sm, ss, dm, ds, flags=B.RESHARD_LDS_STAGING)
+    assert B.reshard_plan_lds_bytes(r) > 0
+    host_case(shape, dt, sm, ss, dm, ds, flags=B.RESHARD_LDS_STAGING, chunk_bytes=chunk)
+
+
+def test_aligned_workloads_do_not_realign():
+    for w in WORKLOADS.values():
+        p = plan_of(w.shape, w.dtype, w.src_mesh, w.src_spec, w.dst_mesh, w.dst_spec)
+        assert B.reshard_plan_realign_chunks(p) == 0
+        assert B.reshard_plan_lds_bytes(p) == 0
+
+
 # ------------------------------------------------------------------ errors
 
 @pytest.mark.parametrize("args,status", [

@@ -235,3 +235,35 @@ def test_workload_full_size(wid):
         assert g.shape == wnt.shape
         assert np.array_equal(g, wnt), f"workload {wid} destination {k} differs"
     _say(f"workload {wid} ok")
+
+
+# ------------------------------------------------------ LDS realignment path
+
+from tests.test_capi_host import REALIGN_CASES  # noqa: E402
+
+
+@pytest.mark.parametrize("case", REALIGN_CASES)
+def test_realign_path(case):
+    shape, dt, sm, ss, dm, ds = case
+    _say(f"realign {case}")
+    assert B.reshard_plan_realign_chunks(B.reshard_plan(shape, dt, sm, ss, dm, ds)) > 0
+    for kw in ({}, {"chunk_bytes": 100, "block_threads": 64}, {"chunk_bytes": 5000, "block_threads": 1024},
+               {"max_wgs_per_cu": -1}, {"flags": B.RESHARD_TASK_ORDER | B.RESHARD_XCD_REMAP},
+               {"flags": B.RESHARD_NO_REALIGN}, {"flags": B.RESHARD_LDS_STAGING},
+               {"flags": B.RESHARD_LDS_STAGING, "chunk_bytes": 300, "block_threads": 64}):
+        got, want = run_gpu(shape, dt, sm, ss, dm, ds, rand_bits(shape, dt, 5), **kw)
+        assert_same(got, want)
+
+
+def test_realign_uneven_large():
+    # fp16 [4, 512, 12300] over 32 shards of the last dim (385 or 384 wide):
+    # every row phase differs between the two layouts; mixed direct and
+    # realignment chunks in one execute
+    shape = (4, 512, 12300)
+    sm, ss, dm, ds = (4, 8), "RRS^{01}", (4, 8), "RS^1R"
+    _say("realign uneven large")
+    p = B.reshard_plan(shape, "float16", sm, ss, dm, ds)
+    assert B.reshard_plan_realign_chunks(p) > 0
+    for flags in (0, B.RESHARD_LDS_STAGING):
+        got, want = run_gpu(shape, "float16", sm, ss, dm, ds, rand_bits(shape, "float16", 6), flags=flags)
+        assert_same(got, want)
