@@ -84,7 +84,10 @@ def main():
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=50)
     ap.add_argument("--warmup", type=int, default=5)
-    ap.add_argument("--config", type=int, default=None, help="workload id 1..5 (default 5)")
+    ap.add_argument("--config", default=None,
+                    help="workload id 1..5 (default 5), or fanoutR (1 GiB, one sender to R replicas)")
+    ap.add_argument("--strategy", choices=["broadcast", "sendrecv", "allgather"], default="broadcast",
+                    help="broadcast (default) or a comparison strategy that re-reads slices per receiver")
     ap.add_argument("--seed", type=int, default=0)
     ap.add_argument("--chunk-bytes", type=int, default=0)
     ap.add_argument("--block-threads", type=int, default=0)
@@ -105,10 +108,11 @@ def main():
     import torch
 
     from paper_2211_05322_amd import binding as B
-    from paper_2211_05322_amd.workloads import BENCH_WORKLOAD, WORKLOADS, make_workload_tensor
+    from paper_2211_05322_amd.workloads import BENCH_WORKLOAD, make_workload_tensor, workload_by_name
 
-    wid = args.config or BENCH_WORKLOAD
-    w = WORKLOADS[wid]
+    w = workload_by_name(args.config or BENCH_WORKLOAD)
+    flags = args.flags | {"broadcast": 0, "sendrecv": B.RESHARD_STRATEGY_SENDRECV,
+                          "allgather": B.RESHARD_STRATEGY_ALLGATHER}[args.strategy]
     if not torch.cuda.is_available():
         print("no GPU visible", file=sys.stderr)
         sys.exit(1)
@@ -129,7 +133,7 @@ def main():
 
     t0 = time.perf_counter()
     plan = B.reshard_plan(w.shape, w.dtype, w.src_mesh, w.src_spec, w.dst_mesh, w.dst_spec,
-                          flags=args.flags, chunk_bytes=args.chunk_bytes, block_threads=args.block_threads)
+                          flags=flags, chunk_bytes=args.chunk_bytes, block_threads=args.block_threads)
     plan_us = (time.perf_counter() - t0) * 1e6
     st = B.reshard_plan_stats(plan)
     dst = B.empty_shards(plan, 1)
@@ -213,7 +217,7 @@ def main():
             "workload": w.name, "shape": list(w.shape), "src_mesh": list(w.src_mesh), "src_spec": w.src_spec,
             "dst_mesh": list(w.dst_mesh), "dst_spec": w.dst_spec, "bytes_read": st["bytes_read"],
             "bytes_written": st["bytes_written"], "unit_tasks": st["n_unit_tasks"],
-            "workgroups": st["n_descriptors"], "max_fanout": st["max_fanout"],
+            "workgroups": st["n_descriptors"], "max_fanout": st["max_fanout"], "strategy": args.strategy,
         },
         "pct_of_hbm_peak": round(100.0 * gbs / HBM_PEAK_GBS, 2),
         "roofline": {

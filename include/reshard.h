@@ -78,6 +78,15 @@ typedef enum {
                                       (default: two overlapping aligned loads per slot,
                                       funnel-shifted in registers). */
 
+/* Comparison strategies (Section 3.1), for measuring what broadcast saves; at
+ * most one.  Both read every slice once per receiver (R x the bytes of D) and
+ * copy rows directly (no realignment path).  Default: broadcast, one read and
+ * one write per receiver in one launch. */
+#define RESHARD_STRATEGY_SENDRECV 0x20u   /* the sender's slice is re-read for each receiver */
+#define RESHARD_STRATEGY_ALLGATHER 0x40u  /* send/recv + all-gather: chunks go round-robin to the
+                                             receivers, then (second launch) each receiver pulls
+                                             the chunks it lacks from the receiver holding them */
+
 /* Compiled limits (RESHARD_EUNSUPPORTED beyond them). */
 #define RESHARD_MAX_NDIM 8
 #define RESHARD_MAX_MESH_NDIM 8
@@ -160,7 +169,7 @@ reshard_status_t reshard_plan_local_shape(const reshard_plan_t *plan, int side, 
 
 /* Plan totals (any output pointer may be NULL):
  *  bytes_read    = bytes of D, each unique slice read once (the lower bound of
- *                  Section 2.2);
+ *                  Section 2.2) -- or R x that under a comparison strategy;
  *  bytes_written = sum of all destination shard sizes (replicas counted);
  *  n_unit_tasks, n_descriptors (workgroup chunks), max_fanout (largest
  *  receiver count of a unit task). */

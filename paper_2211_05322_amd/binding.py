@@ -22,6 +22,8 @@ RESHARD_XCD_REMAP = 0x2
 RESHARD_TASK_ORDER = 0x4
 RESHARD_NO_REALIGN = 0x8
 RESHARD_LDS_STAGING = 0x10
+RESHARD_STRATEGY_SENDRECV = 0x20
+RESHARD_STRATEGY_ALLGATHER = 0x40
 RESHARD_MAX_BUFFERS = 496
 
 _DTYPES = {"uint8": 0, "int8": 1, "float16": 2, "bfloat16": 3, "float32": 4, "int32": 5,

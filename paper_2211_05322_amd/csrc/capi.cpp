@@ -73,8 +73,11 @@ reshard_status_t make_plan(int ndim, const int64_t *shape, reshard_dtype_t dtype
         if (!mul_ok(total, shape[i], int64_t(1) << 56, total))
             return fail(RESHARD_EUNSUPPORTED, "tensor larger than 2^56 bytes");
     }
-    if (flags & ~(RESHARD_SENDER_NAIVE | RESHARD_XCD_REMAP | RESHARD_TASK_ORDER | RESHARD_NO_REALIGN | RESHARD_LDS_STAGING))
+    if (flags & ~(RESHARD_SENDER_NAIVE | RESHARD_XCD_REMAP | RESHARD_TASK_ORDER | RESHARD_NO_REALIGN |
+                  RESHARD_LDS_STAGING | RESHARD_STRATEGY_SENDRECV | RESHARD_STRATEGY_ALLGATHER))
         return fail(RESHARD_EINVAL, "unknown flag bits");
+    if ((flags & RESHARD_STRATEGY_SENDRECV) && (flags & RESHARD_STRATEGY_ALLGATHER))
+        return fail(RESHARD_EINVAL, "at most one strategy flag");
     rs::Tuning tn;
     if (tuning) {
         for (int r : tuning->reserved)
@@ -252,7 +255,11 @@ reshard_status_t reshard_debug_execute_host(const reshard_plan_t *plan, void *co
     for (const rs::Desc &d : p->descs) {
         const uint32_t w = 1u << rs::kind_log2w(d.kind);
         const uint32_t levels = rs::kind_levels(d.kind);
-        const char *src = static_cast<const char *>(src_ptrs[d.src_buf]) + d.src_base;
+        // a source index past the source mesh names a destination buffer
+        // (the all-gather strategy's second phase)
+        const int64_t sbuf = int64_t(d.src_buf);
+        const char *src = static_cast<const char *>(sbuf < p->src.ndev ? src_ptrs[sbuf] : dst_ptrs[sbuf - p->src.ndev]) +
+                          d.src_base;
         if (rs::kind_realign(d.kind) && !(p->flags & RESHARD_LDS_STAGING)) {
             // The kernel's shifted-load realignment, same arithmetic: every
             // loaded word must hold a byte of its row.

@@ -531,8 +531,15 @@ reshard_status_t launch(const Plan &p, const Desc *descs, const int32_t *fan, vo
     const uint32_t cap_lds =
         p.tuning.max_wgs_per_cu ? (160u * 1024u / uint32_t(p.tuning.max_wgs_per_cu)) & ~1023u : 0u;
     const uint32_t n_direct = uint32_t(p.n_direct), n_realign = uint32_t(p.descs.size() - p.n_direct);
-    if (n_direct) {
-        const reshard_status_t st = launch_one(reshard_kernel<NPTR>, a, n_direct, remap, block, cap_lds, stream);
+    const uint32_t n_phase1 = uint32_t(p.n_phase1);
+    if (n_phase1) {
+        const reshard_status_t st = launch_one(reshard_kernel<NPTR>, a, n_phase1, remap, block, cap_lds, stream);
+        if (st != RESHARD_OK) return st;
+    }
+    if (n_direct > n_phase1) {  // second phase, stream-ordered after the first
+        a.descs = descs + n_phase1;
+        const reshard_status_t st =
+            launch_one(reshard_kernel<NPTR>, a, n_direct - n_phase1, remap, block, cap_lds, stream);
         if (st != RESHARD_OK) return st;
     }
     if (n_realign) {

@@ -510,7 +510,8 @@ void lower(Plan &p) {
                 }
                 at += len;
             }
-        } else if (run >= kRealignMinRun && !(p.flags & 0x8u)) {  // 0x8: RESHARD_NO_REALIGN
+        } else if (run >= kRealignMinRun && !(p.flags & 0x8u) && !(p.flags & 0x60u)) {
+            // (0x8: RESHARD_NO_REALIGN; 0x60: a comparison strategy, direct chunks only)
             // different 16-byte phases: stage rows through LDS, segments of
             // at most kRealignSeg bytes
             for (int64_t at = 0; at < run; at += kRealignSeg) {
@@ -540,6 +541,57 @@ void lower(Plan &p) {
     std::stable_partition(p.descs.begin(), p.descs.end(), [](const Desc &d) { return !kind_realign(d.kind); });
     p.n_direct = 0;
     while (p.n_direct < p.descs.size() && !kind_realign(p.descs[p.n_direct].kind)) ++p.n_direct;
+    p.n_phase1 = p.n_direct;
+    if (p.flags & 0x20u) {
+        // Send/recv analogue (Section 3.1): the sender's slice is read once
+        // per receiver -- every chunk becomes one fan-out-1 chunk per receiver.
+        std::vector<Desc> out;
+        out.reserve(p.descs.size() * size_t(std::max<int64_t>(1, p.max_fanout)));
+        for (const Desc &d : p.descs)
+            for (uint32_t k = 0; k < d.nfan; ++k) {
+                Desc e = d;
+                e.fan_off = d.fan_off + k;
+                e.nfan = 1;
+                out.push_back(e);
+            }
+        p.descs.swap(out);
+        p.n_direct = p.n_phase1 = p.descs.size();
+        p.bytes_read = 0;
+        for (const auto &t : p.tasks)
+            p.bytes_read += t.bytes * (p.dst.shard_devs_off[t.dst_shard + 1] - p.dst.shard_devs_off[t.dst_shard]);
+    } else if (p.flags & 0x40u) {
+        // Send/recv + all-gather analogue (Section 3.1): phase 1 hands the
+        // slice's chunks round-robin to its receivers (each part read once
+        // from the sender); phase 2 has every receiver pull the parts it
+        // lacks from the receiver that holds them (a second launch).
+        std::vector<Desc> ph1, ph2;
+        uint64_t c = 0;
+        for (const Desc &d : p.descs) {
+            const uint32_t owner = uint32_t(c++ % d.nfan);
+            Desc e = d;
+            e.fan_off = d.fan_off + owner;
+            e.nfan = 1;
+            ph1.push_back(e);
+            for (uint32_t k = 0; k < d.nfan; ++k) {
+                if (k == owner) continue;
+                Desc g = d;  // same offsets: replicas share one local layout
+                g.src_buf = uint16_t(p.src.ndev + p.fan[d.fan_off + owner]);
+                g.src_base = d.dst_base;
+                g.src_rel0 = d.dst_rel0;
+                for (int l = 0; l < 3; ++l) g.ss[l] = d.ds[l];
+                g.fan_off = d.fan_off + k;
+                g.nfan = 1;
+                ph2.push_back(g);
+            }
+        }
+        p.n_phase1 = ph1.size();
+        ph1.insert(ph1.end(), ph2.begin(), ph2.end());
+        p.descs.swap(ph1);
+        p.n_direct = p.descs.size();
+        p.bytes_read = 0;
+        for (const auto &t : p.tasks)
+            p.bytes_read += t.bytes * (p.dst.shard_devs_off[t.dst_shard + 1] - p.dst.shard_devs_off[t.dst_shard]);
+    }
     p.bytes_written = 0;
     p.dst_local_numel.assign(p.dst.ndev, 0);
     p.src_local_numel.assign(p.src.ndev, 0);

@@ -63,6 +63,8 @@ struct Plan {
     bool too_many = false;     // lowering stopped: descriptor table over its cap
     uint32_t lds_bytes = 0;    // LDS the realignment chunks need per workgroup
     size_t n_direct = 0;       // descs[0, n_direct): direct chunks; the rest: realignment chunks
+    size_t n_phase1 = 0;       // descs[0, n_phase1) run before descs[n_phase1, n_direct)
+                               // (two launches; only the all-gather strategy has a second phase)
     std::vector<int64_t> src_local_numel, dst_local_numel;  // per device
 
     // Device copy of [descs | fan], uploaded on the first execute on each HIP

@@ -62,6 +62,24 @@ WORKLOADS = {
 BENCH_WORKLOAD = 5
 
 
+def fanout_workload(receivers, nbytes=1 << 30):
+    """One sender to `receivers` devices, fully replicated on both sides.
+
+    The shape of the paper's single-sender microbenchmark (Section 5.1.1: a
+    1 GB message from one GPU to 1..4 GPUs, replicated specs), as fp16.
+    """
+    return Workload(f"replicate_fp16_{nbytes >> 20}MiB_1to{receivers}", (nbytes // 2,), "float16", "normal",
+                    (1,), "R", (receivers,), "R")
+
+
+def workload_by_name(key):
+    """WORKLOADS id (1..5 or "1".."5") or "fanoutR" (R receivers, 1 GiB)."""
+    key = str(key)
+    if key.startswith("fanout"):
+        return fanout_workload(int(key[len("fanout"):]))
+    return WORKLOADS[int(key)]
+
+
 def make_tensor(shape, dtype, dist, seed, device="cpu"):
     """Seeded logical tensor of the given shape/dtype/distribution.
 

@@ -300,3 +300,29 @@ def test_empty_tensor_and_empty_shards():
     host_case((3, 8), "float32", (4,), "S^0R", (2,), "RS^0")
     p = plan_of((3, 8), "float32", (4,), "S^0R", (2,), "RS^0")
     assert B.reshard_plan_local_shape(p, 0, 3) == (0, 8)
+
+
+# ------------------------------------------ comparison strategies (f2)
+
+@pytest.mark.parametrize("strategy", [B.RESHARD_STRATEGY_SENDRECV, B.RESHARD_STRATEGY_ALLGATHER])
+@pytest.mark.parametrize("case", _fuzz(30, 31))
+def test_host_strategies_fuzz(strategy, case):
+    shape, dt, sm, ss, dm, ds, flags = case
+    host_case(shape, dt, sm, ss, dm, ds, flags | strategy)
+
+
+@pytest.mark.parametrize("strategy", [B.RESHARD_STRATEGY_SENDRECV, B.RESHARD_STRATEGY_ALLGATHER])
+def test_strategy_traffic(strategy):
+    # both comparison strategies read every slice once per receiver
+    for w in WORKLOADS.values():
+        b = B.reshard_plan_stats(plan_of(w.shape, w.dtype, w.src_mesh, w.src_spec, w.dst_mesh, w.dst_spec))
+        s = B.reshard_plan_stats(plan_of(w.shape, w.dtype, w.src_mesh, w.src_spec, w.dst_mesh, w.dst_spec,
+                                         flags=strategy))
+        assert s["bytes_written"] == b["bytes_written"]
+        assert s["bytes_read"] == b["bytes_written"]  # R x |D| (every slice has R receivers)
+
+
+def test_strategy_flags_exclusive():
+    with pytest.raises(B.ReshardError):
+        plan_of((4, 4), "float16", (2,), "RR", (2,), "RR",
+                flags=B.RESHARD_STRATEGY_SENDRECV | B.RESHARD_STRATEGY_ALLGATHER)

@@ -267,3 +267,31 @@ def test_realign_uneven_large():
     for flags in (0, B.RESHARD_LDS_STAGING):
         got, want = run_gpu(shape, "float16", sm, ss, dm, ds, rand_bits(shape, "float16", 6), flags=flags)
         assert_same(got, want)
+
+
+# ------------------------------------------ comparison strategies (f2)
+
+@pytest.mark.parametrize("strategy", [B.RESHARD_STRATEGY_SENDRECV, B.RESHARD_STRATEGY_ALLGATHER])
+@pytest.mark.parametrize("case", _mid_cases(8, 91))
+def test_strategies(strategy, case):
+    shape, dt, sm, ss, dm, ds = case
+    _say(f"strategy {strategy} {case}")
+    got, want = run_gpu(shape, dt, sm, ss, dm, ds, rand_bits(shape, dt, 8), flags=strategy)
+    assert_same(got, want)
+
+
+@pytest.mark.parametrize("strategy", [B.RESHARD_STRATEGY_SENDRECV, B.RESHARD_STRATEGY_ALLGATHER])
+def test_strategies_full_size_fanout8(strategy):
+    w = WORKLOADS[3]  # 8 receivers per slice
+    _say(f"strategy {strategy} workload 3")
+    x = make_workload_tensor(w, seed=1)
+    xb = as_numpy_bits(x)
+    src = oracle.shard(xb, w.src_mesh, w.src_spec)
+    want = oracle.reshard(src, w.shape, w.src_mesh, w.src_spec, w.dst_mesh, w.dst_spec)
+    p = B.reshard_plan(w.shape, w.dtype, w.src_mesh, w.src_spec, w.dst_mesh, w.dst_spec, flags=strategy)
+    sd = [torch.from_numpy(a).cuda() for a in src]
+    dd = B.empty_shards(p, 1)
+    B.reshard_execute(p, sd, dd)
+    torch.cuda.synchronize()
+    for k, (d, wnt) in enumerate(zip(dd, want)):
+        assert np.array_equal(as_numpy_bits(d), wnt), f"destination {k}"
