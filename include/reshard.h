@@ -215,6 +215,43 @@ reshard_status_t reshard_plan_unit_task(const reshard_plan_t *plan, int64_t inde
 reshard_status_t reshard_debug_execute_host(const reshard_plan_t *plan, void *const *src_ptrs,
                                             void *const *dst_ptrs);
 
+/* Scheduling algorithms of Section 3.2 for the multi-host setting. */
+typedef enum {
+    RESHARD_SCHED_NAIVE = 0,         /* lowest-indexed owner sends; tasks in task order */
+    RESHARD_SCHED_LOAD_BALANCE = 1,  /* Eq. 4 greedy: longest first to the least-loaded host,
+                                        run in that order */
+    RESHARD_SCHED_DFS = 2,           /* depth-first search over (next task, sender host) with
+                                        per-host lower-bound pruning, max_dfs_nodes branches */
+    RESHARD_SCHED_RANDOMIZED = 3,    /* greedy search with randomization: random_rounds random
+                                        orders per step, keep the set busying the most hosts */
+    RESHARD_SCHED_ENSEMBLE = 4       /* the better of DFS and randomized (ties: DFS) */
+} reshard_sched_algo_t;
+
+/*
+ * Choose a sender and a start time for every unit task of `plan` under the
+ * paper's cluster model (Section 3.2, Eq. 1-3): a task occupies its sender
+ * host and all its receiver hosts for its duration; tasks sharing a host do
+ * not overlap; the makespan is minimised.  Device d of the source mesh lives
+ * on host d / src_devices_per_host, of the destination mesh on host
+ * d / dst_devices_per_host (the meshes are disjoint, Section 2.2).  A task's
+ * duration is its slice's byte count (a broadcast takes about one transfer of
+ * the slice, Section 3.1), so times are in bytes at unit bandwidth.
+ *
+ * Host only; does not change the plan (on one GPU every task runs
+ * concurrently in one kernel launch, so order only matters between hosts).
+ * Writes n_unit_tasks entries to sender_out (a source device: the task's
+ * lowest-indexed owner on the chosen host) and start_out, plus the makespan,
+ * a lower bound (no host finishes before the work it must do) and the DFS
+ * branch count.  Any output may be NULL.  random_rounds 0 means 1; seed
+ * drives SplitMix64 (Steele et al., OOPSLA 2014).  EINVAL for NULL plan,
+ * devices per host < 1, negative budgets or an unknown algorithm.
+ */
+reshard_status_t reshard_schedule(const reshard_plan_t *plan, int64_t src_devices_per_host,
+                                  int64_t dst_devices_per_host, reshard_sched_algo_t algo,
+                                  int64_t max_dfs_nodes, int64_t random_rounds, uint64_t seed,
+                                  int64_t *sender_out, int64_t *start_out, int64_t *makespan_out,
+                                  int64_t *lower_bound_out, int64_t *dfs_nodes_out);
+
 /* Text of the last error on the calling thread ("" if none).  Never NULL;
  * valid until the next call on the same thread. */
 const char *reshard_last_error(void);

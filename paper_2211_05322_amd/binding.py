@@ -83,6 +83,10 @@ def load(path=None):
     lib.reshard_plan_unit_task.restype = ctypes.c_int
     lib.reshard_debug_execute_host.argtypes = [ctypes.c_void_p, _VPP, _VPP]
     lib.reshard_debug_execute_host.restype = ctypes.c_int
+    lib.reshard_schedule.argtypes = [ctypes.c_void_p, ctypes.c_int64, ctypes.c_int64, ctypes.c_int,
+                                     ctypes.c_int64, ctypes.c_int64, ctypes.c_uint64,
+                                     _I64P, _I64P, _I64P, _I64P, _I64P]
+    lib.reshard_schedule.restype = ctypes.c_int
     lib.reshard_last_error.argtypes = []
     lib.reshard_last_error.restype = ctypes.c_char_p
     lib.reshard_version.argtypes = []
@@ -233,6 +237,23 @@ def reshard_plan_unit_task(plan, index):
                                          ctypes.byref(nr)))
     return {"box": tuple(zip(tuple(lo), tuple(hi))), "sender": chosen.value,
             "senders": list(snd[:ns.value]), "receivers": list(rcv[:nr.value])}
+
+
+SCHED_ALGOS = {"naive": 0, "load_balance": 1, "dfs": 2, "randomized": 3, "ensemble": 4}
+
+
+def reshard_schedule(plan, src_devices_per_host, dst_devices_per_host, algo="ensemble",
+                     max_dfs_nodes=200000, random_rounds=16, seed=0):
+    """Sender choice and start times under the multi-host model (host-side only)."""
+    n = reshard_plan_stats(plan)["n_unit_tasks"]
+    snd = (ctypes.c_int64 * max(1, n))()
+    st = (ctypes.c_int64 * max(1, n))()
+    mk, lb, nodes = ctypes.c_int64(), ctypes.c_int64(), ctypes.c_int64()
+    _check(load().reshard_schedule(plan.handle, int(src_devices_per_host), int(dst_devices_per_host),
+                                   SCHED_ALGOS[algo], int(max_dfs_nodes), int(random_rounds), int(seed),
+                                   snd, st, ctypes.byref(mk), ctypes.byref(lb), ctypes.byref(nodes)))
+    return {"senders": list(snd[:n]), "starts": list(st[:n]), "makespan": mk.value,
+            "lower_bound": lb.value, "dfs_nodes": nodes.value}
 
 
 def reshard_last_error():

@@ -62,6 +62,24 @@ WORKLOADS = {
 BENCH_WORKLOAD = 5
 
 
+# The multi-to-multi microbenchmark of the paper's Table 3: tensor
+# (1024, 1024, 512), (case, send spec, recv spec, send mesh, recv mesh); a
+# mesh row is one node.  Table 3 prints case 1's send mesh as "(2.4)" and case
+# 5's receive spec as "S_{0}RR"; they are read as (2,4) and S^0RR.
+TABLE3_SHAPE = (1024, 1024, 512)
+TABLE3_CASES = [
+    (1, "S^0RR", "S^0RR", (2, 4), (2, 4)),
+    (2, "RRR", "S^0RR", (2, 4), (2, 4)),
+    (3, "RS^0R", "S^0RR", (2, 4), (2, 4)),
+    (4, "RS^{01}R", "S^{01}RR", (2, 4), (2, 4)),
+    (5, "S^1RR", "S^0RR", (2, 4), (2, 4)),
+    (6, "S^0RR", "S^0RR", (2, 4), (3, 4)),
+    (7, "S^1RR", "RRR", (1, 4), (2, 4)),
+    (8, "RRR", "RRR", (2, 3), (3, 2)),
+    (9, "RS^0R", "RRS^0", (2, 4), (2, 4)),
+]
+
+
 def fanout_workload(receivers, nbytes=1 << 30):
     """One sender to `receivers` devices, fully replicated on both sides.
 
