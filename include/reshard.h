@@ -252,6 +252,26 @@ reshard_status_t reshard_schedule(const reshard_plan_t *plan, int64_t src_device
                                   int64_t *sender_out, int64_t *start_out, int64_t *makespan_out,
                                   int64_t *lower_bound_out, int64_t *dfs_nodes_out);
 
+/*
+ * Latency of one training iteration under the pipeline schedules of Section
+ * 4, with cross-mesh resharding between stages: `stages` stages run
+ * `microbatches` micro-batches; stage s (0-based) runs w forwards, then
+ * alternately one backward and one forward, then the remaining backwards,
+ * with w = stages - s (1F1B, eager = 0) or w = 2(stages - s) - 1
+ * (eager-1F1B, eager = 1), capped at microbatches.  A forward needs the
+ * previous stage's forward of the same micro-batch plus a transfer of
+ * t_comm_fwd; a backward needs the next stage's backward plus t_comm_bwd (the
+ * last stage's backward follows its own forward).  Transfers overlap with
+ * computation; with serial_links != 0 transfers on one directed stage pair go
+ * one at a time.  Writes the latency and, per stage, the peak number of
+ * micro-batches whose forward is done and backward is not (stages entries).
+ * Host only.  EINVAL for stages or microbatches < 1 or a negative time.
+ */
+reshard_status_t reshard_pipeline_simulate(int32_t stages, int32_t microbatches, int32_t eager,
+                                           double t_fwd, double t_bwd, double t_comm_fwd,
+                                           double t_comm_bwd, int32_t serial_links,
+                                           double *latency_out, int32_t *peak_live_out);
+
 /* Text of the last error on the calling thread ("" if none).  Never NULL;
  * valid until the next call on the same thread. */
 const char *reshard_last_error(void);

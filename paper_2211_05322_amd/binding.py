@@ -87,6 +87,10 @@ def load(path=None):
                                      ctypes.c_int64, ctypes.c_int64, ctypes.c_uint64,
                                      _I64P, _I64P, _I64P, _I64P, _I64P]
     lib.reshard_schedule.restype = ctypes.c_int
+    lib.reshard_pipeline_simulate.argtypes = [ctypes.c_int32, ctypes.c_int32, ctypes.c_int32, ctypes.c_double,
+                                              ctypes.c_double, ctypes.c_double, ctypes.c_double, ctypes.c_int32,
+                                              ctypes.POINTER(ctypes.c_double), ctypes.POINTER(ctypes.c_int32)]
+    lib.reshard_pipeline_simulate.restype = ctypes.c_int
     lib.reshard_last_error.argtypes = []
     lib.reshard_last_error.restype = ctypes.c_char_p
     lib.reshard_version.argtypes = []
@@ -254,6 +258,18 @@ def reshard_schedule(plan, src_devices_per_host, dst_devices_per_host, algo="ens
                                    snd, st, ctypes.byref(mk), ctypes.byref(lb), ctypes.byref(nodes)))
     return {"senders": list(snd[:n]), "starts": list(st[:n]), "makespan": mk.value,
             "lower_bound": lb.value, "dfs_nodes": nodes.value}
+
+
+def reshard_pipeline_simulate(stages, microbatches, eager, t_fwd, t_bwd, t_comm_fwd, t_comm_bwd=None,
+                              serial_links=True):
+    """(latency, per-stage peak live micro-batches) of one pipelined iteration."""
+    lat = ctypes.c_double()
+    peak = (ctypes.c_int32 * max(1, int(stages)))()
+    _check(load().reshard_pipeline_simulate(int(stages), int(microbatches), int(bool(eager)), float(t_fwd),
+                                            float(t_bwd), float(t_comm_fwd),
+                                            float(t_comm_fwd if t_comm_bwd is None else t_comm_bwd),
+                                            int(bool(serial_links)), ctypes.byref(lat), peak))
+    return lat.value, list(peak[:int(stages)])
 
 
 def reshard_last_error():

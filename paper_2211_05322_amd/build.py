@@ -24,7 +24,7 @@ ARCH = "gfx950"
 COMMON = ["-O3", "-fPIC", "-std=c++17", "-Wall", "-Wextra", "-Wno-unused-parameter"]
 # packed-fp32 instructions are disabled for all device code
 HIP_FLAGS = [f"--offload-arch={ARCH}", "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops"]
-HOST_SOURCES = ["planner.cpp", "capi.cpp", "schedule.cpp"]
+HOST_SOURCES = ["planner.cpp", "capi.cpp", "schedule.cpp", "pipeline.cpp"]
 HIP_SOURCES = ["execute.hip"]
 
 

@@ -1,0 +1,64 @@
+"""Pipeline schedules of Section 4 (1F1B vs eager-1F1B): oracle pins, parity.
+
+Pins (against facts, not the oracle's own formula): with no communication
+both schedules take (M + S - 1)(f + b), the classic 1F1B makespan, and are
+equal (Section 4); the warm-up counts set the peak live activations, and
+eager-1F1B adds at most #stages of them per stage (Section 4, Table 1
+discussion); communication can only lengthen an iteration; eager-1F1B is
+never slower than 1F1B in these settings.  Parity: the library's simulator
+equals the oracle exactly on a grid of settings.
+"""
+
+import itertools
+
+import pytest
+
+from oracle import pipeline as P
+from paper_2211_05322_amd import binding as B
+
+
+@pytest.mark.parametrize("S,M", [(1, 1), (1, 5), (2, 2), (2, 7), (3, 4), (4, 16), (8, 8), (8, 33)])
+@pytest.mark.parametrize("eager", [0, 1])
+def test_no_communication_closed_form(S, M, eager):
+    f, b = 1.0, 2.0
+    lat, _ = P.simulate(S, M, eager, f, b, 0.0, 0.0)
+    assert lat == (M + S - 1) * (f + b)
+
+
+@pytest.mark.parametrize("S,M", [(2, 8), (4, 4), (4, 13), (6, 24)])
+def test_peak_activations(S, M):
+    _, p1 = P.simulate(S, M, 0, 1.0, 2.0, 0.5, 0.5)
+    _, pe = P.simulate(S, M, 1, 1.0, 2.0, 0.5, 0.5)
+    for s in range(S):
+        i = s + 1  # the paper numbers stages from 1
+        assert p1[s] == min(S - i + 1, M)
+        assert pe[s] == min(2 * (S - i) + 1, M)
+        assert pe[s] - p1[s] <= S
+
+
+@pytest.mark.parametrize("S,M,c", itertools.product([2, 4, 8], [4, 16, 32], [0.25, 1.0, 3.0]))
+def test_communication_and_eagerness(S, M, c):
+    base, _ = P.simulate(S, M, 0, 1.0, 2.0, 0.0, 0.0)
+    l1, _ = P.simulate(S, M, 0, 1.0, 2.0, c, c)
+    le, _ = P.simulate(S, M, 1, 1.0, 2.0, c, c)
+    assert l1 > base and le > base
+    assert le <= l1
+    # every stage does M forwards and M backwards
+    assert le >= M * 3.0
+
+
+@pytest.mark.parametrize("S,M,eager,c,serial",
+                         [(S, M, e, c, sr) for S, M in [(1, 3), (2, 5), (4, 8), (5, 17), (8, 32)]
+                          for e in (0, 1) for c in (0.0, 0.3, 1.7) for sr in (True, False)])
+def test_parity_with_library(S, M, eager, c, serial):
+    want = P.simulate(S, M, eager, 1.25, 2.5, c, 0.5 * c, serial)
+    got = B.reshard_pipeline_simulate(S, M, eager, 1.25, 2.5, c, 0.5 * c, serial)
+    assert got[0] == pytest.approx(want[0], rel=0, abs=1e-9)
+    assert got[1] == want[1]
+
+
+def test_pipeline_errors():
+    with pytest.raises(B.ReshardError):
+        B.reshard_pipeline_simulate(0, 4, 0, 1.0, 2.0, 0.0)
+    with pytest.raises(B.ReshardError):
+        B.reshard_pipeline_simulate(2, 4, 0, -1.0, 2.0, 0.0)
