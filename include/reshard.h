@@ -78,6 +78,11 @@ typedef enum {
                                       (default: two overlapping aligned loads per slot,
                                       funnel-shifted in registers). */
 
+#define RESHARD_NO_GATHER 0x100u   /* copy every unit task separately (default: tasks that share
+                                      a receiver set and cut its rows into equal 16-byte-aligned
+                                      column segments are written row by row, one workgroup
+                                      gathering whole destination rows from their senders). */
+
 /* Comparison strategies (Section 3.1), for measuring what broadcast saves; at
  * most one.  Both read every slice once per receiver (R x the bytes of D) and
  * copy rows directly (no realignment path).  Default: broadcast, one read and
@@ -98,8 +103,9 @@ typedef struct {
                                so a large plan has >= 4096 chunks); whole vectors */
     int32_t block_threads;  /* threads per workgroup: 64, 128, 256, 512 or 1024 (default 256) */
     int32_t max_wgs_per_cu; /* cap on resident workgroups per CU, 2..32, enforced by reserving
-                               LDS per workgroup; 0 = default (12 waves per CU, at least 2
-                               workgroups); -1 = no cap */
+                               LDS per workgroup; 0 = default (direct chunks: 12 waves per
+                               CU; row-gather chunks: 64 / fan-out waves, at least 8; never
+                               below 2 workgroups); -1 = no cap */
     int32_t reserved[4];    /* must be zero */
 } reshard_tuning_t;
 
@@ -189,6 +195,11 @@ int64_t reshard_plan_lds_bytes(const reshard_plan_t *plan);
 /* Number of workgroup chunks that realign rows (source and destination in
  * different 16-byte phases), or -1 for a NULL plan. */
 int64_t reshard_plan_realign_chunks(const reshard_plan_t *plan);
+
+/* Number of workgroup chunks that write whole destination rows gathered
+ * from several senders (RESHARD_NO_GATHER turns them off), or -1 for a NULL
+ * plan. */
+int64_t reshard_plan_gather_chunks(const reshard_plan_t *plan);
 
 /*
  * Unit task `index` (0 <= index < n_unit_tasks), in lexicographic order of the

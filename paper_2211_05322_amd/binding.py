@@ -24,6 +24,7 @@ RESHARD_NO_REALIGN = 0x8
 RESHARD_LDS_STAGING = 0x10
 RESHARD_STRATEGY_SENDRECV = 0x20
 RESHARD_STRATEGY_ALLGATHER = 0x40
+RESHARD_NO_GATHER = 0x100
 RESHARD_MAX_BUFFERS = 496
 
 _DTYPES = {"uint8": 0, "int8": 1, "float16": 2, "bfloat16": 3, "float32": 4, "int32": 5,
@@ -76,6 +77,8 @@ def load(path=None):
     lib.reshard_plan_alignment.restype = ctypes.c_int64
     lib.reshard_plan_lds_bytes.argtypes = [ctypes.c_void_p]
     lib.reshard_plan_lds_bytes.restype = ctypes.c_int64
+    lib.reshard_plan_gather_chunks.argtypes = [ctypes.c_void_p]
+    lib.reshard_plan_gather_chunks.restype = ctypes.c_int64
     lib.reshard_plan_realign_chunks.argtypes = [ctypes.c_void_p]
     lib.reshard_plan_realign_chunks.restype = ctypes.c_int64
     lib.reshard_plan_unit_task.argtypes = [ctypes.c_void_p, ctypes.c_int64, _I64P, _I64P, _I64P,
@@ -223,6 +226,10 @@ def reshard_plan_alignment(plan):
 
 def reshard_plan_lds_bytes(plan):
     return int(load().reshard_plan_lds_bytes(plan.handle))
+
+
+def reshard_plan_gather_chunks(plan):
+    return int(load().reshard_plan_gather_chunks(plan.handle))
 
 
 def reshard_plan_realign_chunks(plan):

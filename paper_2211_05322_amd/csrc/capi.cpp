@@ -74,7 +74,7 @@ reshard_status_t make_plan(int ndim, const int64_t *shape, reshard_dtype_t dtype
             return fail(RESHARD_EUNSUPPORTED, "tensor larger than 2^56 bytes");
     }
     if (flags & ~(RESHARD_SENDER_NAIVE | RESHARD_XCD_REMAP | RESHARD_TASK_ORDER | RESHARD_NO_REALIGN |
-                  RESHARD_LDS_STAGING | RESHARD_STRATEGY_SENDRECV | RESHARD_STRATEGY_ALLGATHER))
+                  RESHARD_LDS_STAGING | RESHARD_STRATEGY_SENDRECV | RESHARD_STRATEGY_ALLGATHER | RESHARD_NO_GATHER))
         return fail(RESHARD_EINVAL, "unknown flag bits");
     if ((flags & RESHARD_STRATEGY_SENDRECV) && (flags & RESHARD_STRATEGY_ALLGATHER))
         return fail(RESHARD_EINVAL, "at most one strategy flag");
@@ -93,6 +93,7 @@ reshard_status_t make_plan(int ndim, const int64_t *shape, reshard_dtype_t dtype
         if (bt) tn.block_threads = bt;
         tn.max_wgs_per_cu = cap;
     }
+    tn.cap_is_default = tn.max_wgs_per_cu == 0;
     if (tn.max_wgs_per_cu == 0) {
         // default residency: about 12 waves per CU (fewer concurrent write
         // streams schedule better in HBM), never below 2 workgroups
@@ -211,9 +212,14 @@ int64_t reshard_plan_lds_bytes(const reshard_plan_t *plan) {
     return (p->flags & RESHARD_LDS_STAGING) ? int64_t(p->lds_bytes) : 0;
 }
 
+int64_t reshard_plan_gather_chunks(const reshard_plan_t *plan) {
+    const rs::Plan *p = as_plan(plan);
+    return p ? int64_t(p->n_gather) : -1;
+}
+
 int64_t reshard_plan_realign_chunks(const reshard_plan_t *plan) {
     const rs::Plan *p = as_plan(plan);
-    return p ? int64_t(p->descs.size() - p->n_direct) : -1;
+    return p ? int64_t(p->descs.size() - p->n_direct - p->n_gather) : -1;
 }
 
 reshard_status_t reshard_plan_unit_task(const reshard_plan_t *plan, int64_t index, int64_t *lo, int64_t *hi,
@@ -252,9 +258,33 @@ reshard_status_t reshard_debug_execute_host(const reshard_plan_t *plan, void *co
         if (p->dst_local_numel[k] > 0 && !dst_ptrs[k])
             return fail(RESHARD_EINVAL, "destination buffer " + std::to_string(k) + " is NULL but its shard is not empty");
     std::vector<uint8_t> lds;
-    for (const rs::Desc &d : p->descs) {
+    for (size_t di = 0; di < p->descs.size(); ++di) {
+        const rs::Desc &d = p->descs[di];
         const uint32_t w = 1u << rs::kind_log2w(d.kind);
         const uint32_t levels = rs::kind_levels(d.kind);
+        if (di >= p->n_direct && di < p->n_direct + p->n_gather) {
+            // row-gather chunk: the kernel's slot -> (row, segment) arithmetic
+            const uint32_t spr = d.vpr, sps = d.run;
+            if (d.pad[0] + d.pad[1] > p->segs.size()) return fail(RESHARD_EINVAL, "internal: segment table range");
+            for (uint32_t v = d.v0; v < d.v1; ++v) {
+                const uint32_t row = rs::fastdiv(v, d.mul_vpr, d.sh_vpr), j = v - row * spr;
+                const uint32_t g = rs::fastdiv(j, d.batch, d.pad[2]), jj = j - g * sps;
+                if (g >= d.pad[1]) return fail(RESHARD_EINVAL, "internal: segment index out of range");
+                uint32_t i1 = 0, i2 = 0, i3 = 0;
+                if (levels == 1) rs::row_indices<1>(d, row, i1, i2, i3);
+                else if (levels == 2) rs::row_indices<2>(d, row, i1, i2, i3);
+                else rs::row_indices<3>(d, row, i1, i2, i3);
+                const uint32_t dr = i1 * d.ds[0] + i2 * d.ds[1] + i3 * d.ds[2] + 16u * j - d.dst_rel0;
+                const rs::Seg &sg = p->segs[d.pad[0] + g];
+                const uint32_t sr = i1 * sg.ss[0] + i2 * sg.ss[1] + i3 * sg.ss[2] + 16u * jj;
+                const char *src = static_cast<const char *>(src_ptrs[sg.buf]) + sg.src_base + sr;
+                for (uint32_t r = 0; r < d.nfan; ++r) {
+                    char *dst = static_cast<char *>(dst_ptrs[p->fan[d.fan_off + r]]) + d.dst_base + dr;
+                    std::memcpy(dst, src, 16);
+                }
+            }
+            continue;
+        }
         // a source index past the source mesh names a destination buffer
         // (the all-gather strategy's second phase)
         const int64_t sbuf = int64_t(d.src_buf);

@@ -92,6 +92,46 @@ struct alignas(16) Desc {
 };
 static_assert(sizeof(Desc) == 112, "descriptor layout is shared by host and device");
 
+// Row-gather path.  A row group is the set of unit tasks that share one
+// receiver set and one box in every dimension but the last, and cut the
+// receivers' rows into equal 16-byte-aligned column segments, one per task
+// (each from its own sender).  A gather chunk is a range of 16-byte slots of
+// whole destination rows; slot j of a row belongs to segment j / sps.  Its
+// descriptor uses: vpr = slots per row, run = sps, batch = fast-division
+// multiplier of sps and pad[2] its shift, pad[0] = first segment entry,
+// pad[1] = number of segments; ds[] and dst_base/dst_rel0 as usual.  ss[],
+// src_buf and src_base are unused: every segment entry carries its sender,
+// the 64-bit offset of the group's first row at the segment's first column,
+// and the sender's strides of the outer levels (mod 2^32).  Source offsets
+// are relative to that origin and below 2^32.
+struct Seg {
+    uint64_t src_base;
+    uint32_t ss[3];
+    uint32_t buf;
+};
+static_assert(sizeof(Seg) == 24, "segment entries are shared by host and device");
+constexpr uint32_t kMaxSegs = 256;  // segment entries one gather chunk may stage
+
+// Outer-level indices of a row (level 1 = innermost outer level).
+template <int LEVELS>
+constexpr void row_indices(const Desc &d, uint32_t row, uint32_t &i1, uint32_t &i2, uint32_t &i3) {
+    if (LEVELS == 1) {
+        i1 = row;
+        i2 = 0;
+        i3 = 0;
+    } else {
+        const uint32_t r2 = fastdiv(row, d.mul_n1, d.sh_n1);
+        i1 = row - r2 * d.n1;
+        if (LEVELS == 2) {
+            i2 = r2;
+            i3 = 0;
+        } else {
+            i3 = fastdiv(r2, d.mul_n2, d.sh_n2);
+            i2 = r2 - i3 * d.n2;
+        }
+    }
+}
+
 // Offsets (sender, receiver) of vector v relative to the chunk's first vector.
 struct Rel {
     uint32_t src;

@@ -40,6 +40,7 @@ template <int NPTR>
 struct KArgs {
     const Desc *descs;
     const int32_t *fan;
+    const Seg *segs;   // row-gather segment entries
     uint32_t ndesc;
     uint32_t nsrc;     // ptr[0, nsrc) are source buffers, ptr[nsrc, ...) destination buffers
     uint32_t per_xcd;  // > 0: XCD x runs chunks [x*per_xcd, (x+1)*per_xcd)
@@ -425,6 +426,114 @@ __device__ __forceinline__ void run_shift(const Desc &d, const RS_CONST KArgs<NP
     }
 }
 
+// Row-gather path (see desc.h): a workgroup writes whole destination rows,
+// each 16-byte slot loaded from the sender owning its column segment.  The
+// chunk's segment entries are staged in LDS once (64-bit source pointer +
+// three strides each), then each lane gathers its slots with per-lane
+// pointers; stores are the direct path's (receiver bases in scalar
+// registers, one shared 32-bit offset).
+template <int L, int U, bool FULL>
+__device__ __forceinline__ void gather_batch(const Desc &d, const uint64_t *sp, const uint32_t *sst, uint32_t v,
+                                             uint32_t nthr, uint32_t end, u32x4 (&x)[U], uint32_t (&doff)[U]) {
+#pragma unroll
+    for (int u = 0; u < U; ++u) {
+        const uint32_t vi = v + u * nthr;
+        if (FULL || vi < end) {
+            const uint32_t row = fastdiv(vi, d.mul_vpr, d.sh_vpr);
+            const uint32_t j = vi - row * d.vpr;
+            const uint32_t g = fastdiv(j, d.batch, d.pad[2]);
+            const uint32_t jj = j - g * d.run;
+            uint32_t i1, i2, i3;
+            row_indices<L>(d, row, i1, i2, i3);
+            doff[u] = i1 * d.ds[0] + i2 * d.ds[1] + i3 * d.ds[2] + 16u * j - d.dst_rel0;
+            const uint32_t so = i1 * sst[3 * g] + i2 * sst[3 * g + 1] + i3 * sst[3 * g + 2] + 16u * jj;
+            x[u] = load_vec((const RS_GLOBAL u32x4 *)(sp[g] + so));
+        }
+    }
+}
+
+template <int L, int RF, int NPTR>
+__device__ __forceinline__ void run_gather(const Desc &d, const RS_CONST KArgs<NPTR> *a) {
+    extern __shared__ __attribute__((aligned(16))) unsigned char rs_lds[];
+    constexpr int U = RS_UNROLL;
+    uint64_t *sp = reinterpret_cast<uint64_t *>(rs_lds);
+    uint32_t *sst = reinterpret_cast<uint32_t *>(rs_lds + 8u * kMaxSegs);
+    const uint32_t nthr = blockDim.x, tid = threadIdx.x;
+    const RS_CONST Seg *segs = (const RS_CONST Seg *)(a->segs + d.pad[0]);
+    for (uint32_t g = tid; g < d.pad[1]; g += nthr) {
+        const Seg sg = {segs[g].src_base, {segs[g].ss[0], segs[g].ss[1], segs[g].ss[2]}, segs[g].buf};
+        sp[g] = uint64_t(a->ptr[sg.buf]) + sg.src_base;
+        sst[3 * g] = sg.ss[0];
+        sst[3 * g + 1] = sg.ss[1];
+        sst[3 * g + 2] = sg.ss[2];
+    }
+    __syncthreads();
+    const RS_CONST int32_t *fan = (const RS_CONST int32_t *)(a->fan + d.fan_off);
+    const uint32_t end = d.v1, step = U * nthr;
+    uint32_t base = d.v0;
+    u32x4 x[U], y[U];
+    uint32_t dx[U], dy[U];
+    if (base + step <= end) {
+        gather_batch<L, U, true>(d, sp, sst, base + tid, nthr, end, x, dx);
+        for (;;) {
+            if (base + 2 * step > end) {
+                store_batch<16, U, RF, true>(d, a, fan, base + tid, nthr, end, x, dx);
+                base += step;
+                break;
+            }
+            gather_batch<L, U, true>(d, sp, sst, base + step + tid, nthr, end, y, dy);
+            store_batch<16, U, RF, true>(d, a, fan, base + tid, nthr, end, x, dx);
+            base += step;
+            if (base + 2 * step > end) {
+                store_batch<16, U, RF, true>(d, a, fan, base + tid, nthr, end, y, dy);
+                base += step;
+                break;
+            }
+            gather_batch<L, U, true>(d, sp, sst, base + step + tid, nthr, end, x, dx);
+            store_batch<16, U, RF, true>(d, a, fan, base + tid, nthr, end, y, dy);
+            base += step;
+        }
+    }
+    if (base < end) {
+        gather_batch<L, U, false>(d, sp, sst, base + tid, nthr, end, x, dx);
+        store_batch<16, U, RF, false>(d, a, fan, base + tid, nthr, end, x, dx);
+    }
+}
+
+template <int L, int NPTR>
+__device__ __forceinline__ void run_gather_fan(const Desc &d, const RS_CONST KArgs<NPTR> *a) {
+    switch (d.nfan) {
+        case 1: run_gather<L, 1>(d, a); break;
+        case 2: run_gather<L, 2>(d, a); break;
+        case 3: run_gather<L, 3>(d, a); break;
+        case 4: run_gather<L, 4>(d, a); break;
+        case 5: run_gather<L, 5>(d, a); break;
+        case 6: run_gather<L, 6>(d, a); break;
+        case 7: run_gather<L, 7>(d, a); break;
+        case 8: run_gather<L, 8>(d, a); break;
+        default: run_gather<L, 0>(d, a); break;
+    }
+}
+
+template <int NPTR>
+__global__ __launch_bounds__(1024) void reshard_gather_kernel(KArgs<NPTR> args) {
+    const RS_CONST KArgs<NPTR> *a = (const RS_CONST KArgs<NPTR> *)__builtin_amdgcn_kernarg_segment_ptr();
+    const uint32_t b = blockIdx.x;
+    const uint32_t idx = a->per_xcd ? (b & 7u) * a->per_xcd + (b >> 3) : b;
+    if (idx >= a->ndesc) return;
+    const RS_CONST u32x4 *q = (const RS_CONST u32x4 *)(a->descs + idx);
+    u32x4 raw[sizeof(Desc) / 16];
+#pragma unroll
+    for (int i = 0; i < int(sizeof(Desc) / 16); ++i) raw[i] = q[i];
+    Desc d;
+    __builtin_memcpy(&d, raw, sizeof(Desc));
+    switch (kind_levels(d.kind)) {
+        case 1: run_gather_fan<1>(d, a); break;
+        case 2: run_gather_fan<2>(d, a); break;
+        default: run_gather_fan<3>(d, a); break;
+    }
+}
+
 // Realignment chunks run in their own kernel so their register use does not
 // bound the direct kernel's occupancy.  STAGE: through LDS, else shifted loads.
 template <int NPTR, bool STAGE>
@@ -463,15 +572,17 @@ reshard_status_t hip_fail(const char *what, hipError_t e) {
 }
 
 // Upload [descs | fan] to the current device once; returns the device pointer.
-reshard_status_t device_table(const Plan &p, int dev, const Desc **descs, const int32_t **fan) {
+reshard_status_t device_table(const Plan &p, int dev, const Desc **descs, const int32_t **fan, const Seg **segs) {
     if (dev < 0 || dev >= Plan::kMaxHipDevices)
         return fail(RESHARD_EUNSUPPORTED, "HIP device ordinal " + std::to_string(dev) + " above the plan's limit");
     std::lock_guard<std::mutex> lock(p.mu);
     const size_t dbytes = p.descs.size() * sizeof(Desc);
+    const size_t fbytes = p.fan.size() * sizeof(int32_t);
+    const size_t soff = (dbytes + fbytes + 15) & ~size_t(15);
+    const size_t sbytes = p.segs.size() * sizeof(Seg);
     if (!p.d_table[dev]) {
-        const size_t fbytes = p.fan.size() * sizeof(int32_t);
         void *mem = nullptr;
-        hipError_t e = hipMalloc(&mem, dbytes + fbytes);
+        hipError_t e = hipMalloc(&mem, soff + sbytes);
         if (e != hipSuccess) {
             (void)hipGetLastError();
             return fail(RESHARD_ENOMEM, std::string("hipMalloc of the descriptor table: ") + hipGetErrorString(e));
@@ -479,6 +590,8 @@ reshard_status_t device_table(const Plan &p, int dev, const Desc **descs, const 
         e = hipMemcpy(mem, p.descs.data(), dbytes, hipMemcpyHostToDevice);
         if (e == hipSuccess && fbytes)
             e = hipMemcpy(static_cast<char *>(mem) + dbytes, p.fan.data(), fbytes, hipMemcpyHostToDevice);
+        if (e == hipSuccess && sbytes)
+            e = hipMemcpy(static_cast<char *>(mem) + soff, p.segs.data(), sbytes, hipMemcpyHostToDevice);
         if (e != hipSuccess) {
             (void)hipFree(mem);
             return hip_fail("upload of the descriptor table", e);
@@ -487,6 +600,7 @@ reshard_status_t device_table(const Plan &p, int dev, const Desc **descs, const 
     }
     *descs = static_cast<const Desc *>(p.d_table[dev]);
     *fan = reinterpret_cast<const int32_t *>(static_cast<const char *>(p.d_table[dev]) + dbytes);
+    *segs = reinterpret_cast<const Seg *>(static_cast<const char *>(p.d_table[dev]) + soff);
     return RESHARD_OK;
 }
 
@@ -513,11 +627,12 @@ reshard_status_t launch_one(K kernel, A a, uint32_t ndesc, bool remap, uint32_t 
 }
 
 template <int NPTR>
-reshard_status_t launch(const Plan &p, const Desc *descs, const int32_t *fan, void *const *src_ptrs,
-                        void *const *dst_ptrs, hipStream_t stream) {
+reshard_status_t launch(const Plan &p, const Desc *descs, const int32_t *fan, const Seg *segs,
+                        void *const *src_ptrs, void *const *dst_ptrs, hipStream_t stream) {
     KArgs<NPTR> a;
     a.descs = descs;
     a.fan = fan;
+    a.segs = segs;
     a.ndesc = 0;
     a.nsrc = uint32_t(p.src.ndev);
     a.per_xcd = 0;
@@ -530,7 +645,8 @@ reshard_status_t launch(const Plan &p, const Desc *descs, const int32_t *fan, vo
     // workgroups per CU: the CU holds 160 KiB of LDS.
     const uint32_t cap_lds =
         p.tuning.max_wgs_per_cu ? (160u * 1024u / uint32_t(p.tuning.max_wgs_per_cu)) & ~1023u : 0u;
-    const uint32_t n_direct = uint32_t(p.n_direct), n_realign = uint32_t(p.descs.size() - p.n_direct);
+    const uint32_t n_direct = uint32_t(p.n_direct), n_gather = uint32_t(p.n_gather);
+    const uint32_t n_realign = uint32_t(p.descs.size() - p.n_direct - p.n_gather);
     const uint32_t n_phase1 = uint32_t(p.n_phase1);
     if (n_phase1) {
         const reshard_status_t st = launch_one(reshard_kernel<NPTR>, a, n_phase1, remap, block, cap_lds, stream);
@@ -542,8 +658,28 @@ reshard_status_t launch(const Plan &p, const Desc *descs, const int32_t *fan, vo
             launch_one(reshard_kernel<NPTR>, a, n_direct - n_phase1, remap, block, cap_lds, stream);
         if (st != RESHARD_OK) return st;
     }
-    if (n_realign) {
+    if (n_gather) {
+        // Default residency for the gather kernel: about 64 receiver write
+        // streams per CU (64 / fan-out waves, at least 8 waves) -- measured
+        // best at fan-out 4 and 8.  The segment entries it stages in LDS fit
+        // inside that reservation.
+        uint32_t gcap_lds = cap_lds;
+        if (p.tuning.cap_is_default) {
+            const uint32_t fan = uint32_t(p.gather_fanout > 0 ? p.gather_fanout : 1);
+            uint32_t waves = 64u / fan;
+            if (waves < 8u) waves = 8u;
+            uint32_t wgs = waves / (block / 64u ? block / 64u : 1u);
+            if (wgs < 2u) wgs = 2u;
+            gcap_lds = wgs >= 32u ? 0u : (160u * 1024u / wgs) & ~1023u;
+        }
+        const uint32_t need = (12u + 8u) * kMaxSegs;
         a.descs = descs + n_direct;
+        const reshard_status_t st = launch_one(reshard_gather_kernel<NPTR>, a, n_gather, remap, block,
+                                               gcap_lds > need ? gcap_lds : need, stream);
+        if (st != RESHARD_OK) return st;
+    }
+    if (n_realign) {
+        a.descs = descs + n_direct + n_gather;
         // Realignment kernels hide their load -> shift -> store latency with
         // resident workgroups: no residency cap (measured: capping at 12
         // waves per CU halves their throughput).  Staging takes its LDS.
@@ -603,9 +739,10 @@ extern "C" reshard_status_t reshard_execute(const reshard_plan_t *plan, void *co
     if (e != hipSuccess) return fail(RESHARD_EHIP, std::string("hipGetDevice: ") + hipGetErrorString(e));
     const Desc *descs = nullptr;
     const int32_t *fan = nullptr;
-    reshard_status_t st = device_table(*p, dev, &descs, &fan);
+    const Seg *segs = nullptr;
+    reshard_status_t st = device_table(*p, dev, &descs, &fan, &segs);
     if (st != RESHARD_OK) return st;
     hipStream_t s = static_cast<hipStream_t>(stream);
-    if (p->src.ndev + p->dst.ndev <= 64) return launch<64>(*p, descs, fan, src_ptrs, dst_ptrs, s);
-    return launch<RESHARD_MAX_BUFFERS>(*p, descs, fan, src_ptrs, dst_ptrs, s);
+    if (p->src.ndev + p->dst.ndev <= 64) return launch<64>(*p, descs, fan, segs, src_ptrs, dst_ptrs, s);
+    return launch<RESHARD_MAX_BUFFERS>(*p, descs, fan, segs, src_ptrs, dst_ptrs, s);
 }

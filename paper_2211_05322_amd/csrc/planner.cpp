@@ -2,6 +2,7 @@
 #include "planner.hpp"
 
 #include <algorithm>
+#include <map>
 #include <numeric>
 
 namespace rs {
@@ -435,6 +436,151 @@ int64_t auto_chunk_bytes(int64_t bytes_read) {
 
 }  // namespace
 
+// Row-gather lowering of one group (see desc.h).  Returns false, emitting
+// nothing, when the group does not qualify; its tasks then take the
+// per-task path.
+bool lower_gather_group(Plan &p, const std::vector<size_t> &group, int64_t chunk_bytes, std::vector<Desc> &out) {
+    const int nd = p.ndim;
+    const int64_t es = p.es;
+    if (nd < 1 || group.size() < 2 || group.size() > kMaxSegs) return false;
+    std::vector<size_t> g(group);
+    std::sort(g.begin(), g.end(), [&](size_t a, size_t b) { return p.tasks[a].lo[nd - 1] < p.tasks[b].lo[nd - 1]; });
+    const UnitTask &t0 = p.tasks[g[0]];
+    const int64_t fan_off = p.dst.shard_devs_off[t0.dst_shard];
+    const int64_t nfan = p.dst.shard_devs_off[t0.dst_shard + 1] - fan_off;
+    const int32_t rcv0 = p.dst.shard_devs[fan_off];
+    // destination local layout
+    std::vector<int64_t> ext_d(nd), str_d(nd), dlo(nd);
+    for (int d = 0; d < nd; ++d) {
+        const int64_t jd = p.dst.dev_shard[int64_t(rcv0) * nd + d];
+        dlo[d] = p.dst.bounds[d][jd];
+        ext_d[d] = p.dst.bounds[d][jd + 1] - dlo[d];
+    }
+    for (int d = nd - 1; d >= 0; --d) str_d[d] = d == nd - 1 ? es : str_d[d + 1] * ext_d[d + 1];
+    // the segments must tile the destination row with equal, 16-byte widths
+    const int64_t wcol = t0.hi[nd - 1] - t0.lo[nd - 1];
+    int64_t at = dlo[nd - 1];
+    for (size_t k : g) {
+        const UnitTask &t = p.tasks[k];
+        if (t.lo[nd - 1] != at || t.hi[nd - 1] - t.lo[nd - 1] != wcol) return false;
+        at = t.hi[nd - 1];
+    }
+    if (at != dlo[nd - 1] + ext_d[nd - 1]) return false;
+    const int64_t seg_bytes = wcol * es, row_bytes = ext_d[nd - 1] * es;
+    if (seg_bytes % 16 || row_bytes % 16) return false;
+    // outer levels: drop unit extents, merge dims contiguous on the
+    // destination and on every sender
+    const size_t ns = g.size();
+    std::vector<std::vector<int64_t>> str_s(ns, std::vector<int64_t>(nd)), slo(ns, std::vector<int64_t>(nd));
+    for (size_t k = 0; k < ns; ++k) {
+        const UnitTask &t = p.tasks[g[k]];
+        std::vector<int64_t> ext_s(nd);
+        for (int d = 0; d < nd; ++d) {
+            const int64_t js = p.src.dev_shard[int64_t(t.sender) * nd + d];
+            slo[k][d] = p.src.bounds[d][js];
+            ext_s[d] = p.src.bounds[d][js + 1] - slo[k][d];
+        }
+        for (int d = nd - 1; d >= 0; --d) str_s[k][d] = d == nd - 1 ? es : str_s[k][d + 1] * ext_s[d + 1];
+    }
+    struct GLevel {
+        int64_t n, ds;
+        std::vector<int64_t> ss;
+    };
+    std::vector<GLevel> lv;  // innermost first while building
+    for (int d = nd - 2; d >= 0; --d) {
+        const int64_t n = t0.hi[d] - t0.lo[d];
+        if (n == 1) continue;
+        bool merge = !lv.empty() && str_d[d] == lv.back().n * lv.back().ds;
+        for (size_t k = 0; k < ns && merge; ++k) merge = str_s[k][d] == lv.back().n * lv.back().ss[k];
+        if (merge) {
+            lv.back().n *= n;
+        } else {
+            GLevel l{n, str_d[d], std::vector<int64_t>(ns)};
+            for (size_t k = 0; k < ns; ++k) l.ss[k] = str_s[k][d];
+            lv.push_back(l);
+        }
+    }
+    if (lv.size() > 3) return false;
+    for (const auto &l : lv) {
+        if (l.ds % 16) return false;
+        for (int64_t x : l.ss)
+            if (x % 16) return false;
+    }
+    uint64_t rows = 1;
+    for (const auto &l : lv) rows *= uint64_t(l.n);
+    const uint64_t spr = uint64_t(row_bytes / 16), sps = uint64_t(seg_bytes / 16);
+    if (rows * spr >= (uint64_t(1) << 31)) return false;
+    // per-segment source origin and span (relative offsets stay below 2^32)
+    std::vector<Seg> seg(ns);
+    for (size_t k = 0; k < ns; ++k) {
+        const UnitTask &t = p.tasks[g[k]];
+        uint64_t so = 0, span = uint64_t(seg_bytes);
+        for (int d = 0; d < nd; ++d) so += uint64_t((t.lo[d] - slo[k][d]) * str_s[k][d]);
+        if (so % 16) return false;
+        for (const auto &l : lv) span += uint64_t(l.n - 1) * uint64_t(l.ss[k]);
+        if (span >= (uint64_t(1) << 32)) return false;
+        seg[k].src_base = so;
+        seg[k].buf = uint32_t(t.sender);
+        for (size_t i = 0; i < lv.size(); ++i) seg[k].ss[i] = uint32_t(uint64_t(lv[i].ss[k]));
+    }
+    uint64_t dso = 0;
+    for (int d = 0; d < nd - 1; ++d) dso += uint64_t((t0.lo[d] - dlo[d]) * str_d[d]);
+    const int levels = std::max<int>(1, int(lv.size()));
+    Desc d{};
+    for (size_t i = 0; i < lv.size(); ++i) d.ds[i] = uint32_t(uint64_t(lv[i].ds));
+    d.vpr = uint32_t(spr);
+    d.n1 = lv.size() >= 2 ? uint32_t(lv[0].n) : 1u;
+    d.n2 = lv.size() >= 3 ? uint32_t(lv[1].n) : 1u;
+    const FastDiv f0 = make_fastdiv(d.vpr), f1 = make_fastdiv(d.n1), f2 = make_fastdiv(d.n2),
+                  fs = make_fastdiv(uint32_t(sps));
+    d.mul_vpr = f0.mul; d.sh_vpr = uint8_t(f0.shift);
+    d.mul_n1 = f1.mul;  d.sh_n1 = uint8_t(f1.shift);
+    d.mul_n2 = f2.mul;  d.sh_n2 = uint8_t(f2.shift);
+    d.run = uint32_t(sps);
+    d.batch = fs.mul;
+    d.pad[2] = fs.shift;
+    d.kind = uint8_t(make_kind(4, uint32_t(levels)));
+    d.nfan = uint16_t(nfan);
+    d.fan_off = uint32_t(fan_off);
+    d.pad[0] = uint32_t(p.segs.size());
+    d.pad[1] = uint32_t(ns);
+    // destination offset of slot v of the group (64-bit), levels innermost first
+    auto dst_off = [&](uint64_t v) {
+        uint64_t row = v / spr, off = dso + (v - row * spr) * 16;
+        for (size_t i = 0; i < lv.size(); ++i) {
+            const uint64_t n = uint64_t(lv[i].n);
+            const uint64_t idx = i + 1 == lv.size() ? row : row % n;
+            off += idx * uint64_t(lv[i].ds);
+            row = i + 1 == lv.size() ? 0 : row / n;
+        }
+        return off;
+    };
+    uint64_t cv = uint64_t(std::max<int64_t>(16, chunk_bytes / 16)) / 16 * 16;
+    const uint64_t total = rows * spr;
+    if (p.descs.size() + out.size() + (total + cv - 1) / cv > kMaxDescs) {
+        p.too_many = true;
+        return false;
+    }
+    std::vector<Desc> mine;
+    for (uint64_t v0 = 0; v0 < total;) {
+        uint64_t v1 = std::min(total, v0 + cv);
+        const uint64_t first = dst_off(v0);
+        while (dst_off(v1 - 1) + 16 - first >= kMaxChunkSpan) v1 = v0 + (v1 - v0) / 2;
+        d.v0 = uint32_t(v0);
+        d.v1 = uint32_t(v1);
+        d.dst_base = first;
+        d.dst_rel0 = uint32_t(first - dso);
+        mine.push_back(d);
+        v0 = v1;
+    }
+    p.segs.insert(p.segs.end(), seg.begin(), seg.end());
+    out.insert(out.end(), mine.begin(), mine.end());
+    p.align = std::max<int64_t>(p.align, 16);
+    p.max_fanout = std::max(p.max_fanout, nfan);
+    p.gather_fanout = std::max(p.gather_fanout, nfan);
+    return true;
+}
+
 void lower(Plan &p) {
     const int nd = p.ndim;
     const int64_t es = p.es;
@@ -448,8 +594,32 @@ void lower(Plan &p) {
     for (const auto &t : p.tasks) p.bytes_read += t.bytes;
     const int64_t chunk = p.tuning.chunk_bytes > 0 ? p.tuning.chunk_bytes : auto_chunk_bytes(p.bytes_read);
 
+    // Row groups: tasks sharing the receiver set and the box in every
+    // dimension but the last (0x100: RESHARD_NO_GATHER; strategies copy per task).
+    p.segs.clear();
+    p.gather_fanout = 0;
+    std::vector<Desc> gdescs;
+    std::vector<char> handled(p.tasks.size(), 0);
+    if (!(p.flags & 0x100u) && !(p.flags & 0x60u)) {
+        std::map<std::vector<int64_t>, std::vector<size_t>> groups;
+        for (size_t i = 0; i < p.tasks.size(); ++i) {
+            const UnitTask &t = p.tasks[i];
+            std::vector<int64_t> key{t.dst_shard};
+            for (int d = 0; d + 1 < nd; ++d) {
+                key.push_back(t.lo[d]);
+                key.push_back(t.hi[d]);
+            }
+            groups[key].push_back(i);
+        }
+        for (const auto &kv : groups)
+            if (lower_gather_group(p, kv.second, chunk, gdescs))
+                for (size_t i : kv.second) handled[i] = 1;
+    }
+
     std::vector<int64_t> ext_s(nd), ext_d(nd), str_s(nd), str_d(nd);
-    for (const auto &t : p.tasks) {
+    for (size_t ti = 0; ti < p.tasks.size(); ++ti) {
+        if (handled[ti]) continue;
+        const auto &t = p.tasks[ti];
         const int64_t fan_off = p.dst.shard_devs_off[t.dst_shard];
         const int64_t nfan = p.dst.shard_devs_off[t.dst_shard + 1] - fan_off;
         p.max_fanout = std::max(p.max_fanout, nfan);
@@ -537,10 +707,13 @@ void lower(Plan &p) {
         for (size_t i = 0; i < key.size(); ++i) sorted[i] = p.descs[key[i].second];
         p.descs.swap(sorted);
     }
-    // direct chunks first, realignment chunks last (two kernels)
+    // direct chunks first, then row-gather chunks, realignment chunks last
+    // (three kernels)
     std::stable_partition(p.descs.begin(), p.descs.end(), [](const Desc &d) { return !kind_realign(d.kind); });
     p.n_direct = 0;
     while (p.n_direct < p.descs.size() && !kind_realign(p.descs[p.n_direct].kind)) ++p.n_direct;
+    p.descs.insert(p.descs.begin() + std::ptrdiff_t(p.n_direct), gdescs.begin(), gdescs.end());
+    p.n_gather = gdescs.size();
     p.n_phase1 = p.n_direct;
     if (p.flags & 0x20u) {
         // Send/recv analogue (Section 3.1): the sender's slice is read once

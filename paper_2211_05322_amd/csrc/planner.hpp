@@ -46,6 +46,7 @@ struct Tuning {
     int64_t chunk_bytes = 0;   // 0: automatic
     int32_t block_threads = 256;
     int32_t max_wgs_per_cu = 0;  // resolved cap (0: none)
+    bool cap_is_default = true;  // the caller left the cap to the library
 };
 
 struct Plan {
@@ -62,7 +63,11 @@ struct Plan {
     int64_t align = 1;         // required buffer alignment in bytes
     bool too_many = false;     // lowering stopped: descriptor table over its cap
     uint32_t lds_bytes = 0;    // LDS the realignment chunks need per workgroup
-    size_t n_direct = 0;       // descs[0, n_direct): direct chunks; the rest: realignment chunks
+    size_t n_direct = 0;       // descs[0, n_direct): direct chunks
+    size_t n_gather = 0;       // descs[n_direct, n_direct + n_gather): row-gather chunks;
+                               // the rest: realignment chunks
+    std::vector<Seg> segs;     // row-gather segment entries
+    int64_t gather_fanout = 0; // largest receiver count among row-gather chunks
     size_t n_phase1 = 0;       // descs[0, n_phase1) run before descs[n_phase1, n_direct)
                                // (two launches; only the all-gather strategy has a second phase)
     std::vector<int64_t> src_local_numel, dst_local_numel;  // per device

@@ -326,3 +326,32 @@ def test_strategy_flags_exclusive():
     with pytest.raises(B.ReshardError):
         plan_of((4, 4), "float16", (2,), "RR", (2,), "RR",
                 flags=B.RESHARD_STRATEGY_SENDRECV | B.RESHARD_STRATEGY_ALLGATHER)
+
+
+# ------------------------------------------------------------ row gather
+
+GATHER_CASES = [
+    ((8, 64, 1024), "float16", (2, 4), "RRS^{01}", (2, 4), "RS^0R"),
+    ((3, 40, 640), "float32", (1, 4), "RRS^1", (2,), "RRR"),
+    ((6, 8, 10, 256), "float16", (2, 2), "RRRS^{01}", (3,), "RS^0RR"),
+    ((16, 4, 96), "float64", (3,), "RRS^0", (2, 2), "S^0RR"),
+    ((2, 64, 1024), "float16", (4, 8), "RRS^{01}", (4, 8), "RS^1R"),
+]
+
+
+@pytest.mark.parametrize("case", GATHER_CASES)
+@pytest.mark.parametrize("chunk", [0, 256, 3000])
+def test_host_gather(case, chunk):
+    shape, dt, sm, ss, dm, ds = case
+    p = plan_of(shape, dt, sm, ss, dm, ds, chunk_bytes=chunk)
+    assert B.reshard_plan_gather_chunks(p) > 0, "case should take the row-gather path"
+    host_case(shape, dt, sm, ss, dm, ds, chunk_bytes=chunk)
+    q = plan_of(shape, dt, sm, ss, dm, ds, flags=B.RESHARD_NO_GATHER)
+    assert B.reshard_plan_gather_chunks(q) == 0
+    host_case(shape, dt, sm, ss, dm, ds, flags=B.RESHARD_NO_GATHER)
+
+
+def test_gather_used_by_column_split_workloads():
+    for wid, w in WORKLOADS.items():
+        p = plan_of(w.shape, w.dtype, w.src_mesh, w.src_spec, w.dst_mesh, w.dst_spec)
+        assert (B.reshard_plan_gather_chunks(p) > 0) == (wid in (3, 5)), wid

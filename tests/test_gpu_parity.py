@@ -295,3 +295,19 @@ def test_strategies_full_size_fanout8(strategy):
     torch.cuda.synchronize()
     for k, (d, wnt) in enumerate(zip(dd, want)):
         assert np.array_equal(as_numpy_bits(d), wnt), f"destination {k}"
+
+
+# ------------------------------------------------------------ row gather
+
+from tests.test_capi_host import GATHER_CASES  # noqa: E402
+
+
+@pytest.mark.parametrize("case", GATHER_CASES)
+def test_gather_path(case):
+    shape, dt, sm, ss, dm, ds = case
+    _say(f"gather {case}")
+    assert B.reshard_plan_gather_chunks(B.reshard_plan(shape, dt, sm, ss, dm, ds)) > 0
+    for kw in ({}, {"chunk_bytes": 256, "block_threads": 64}, {"chunk_bytes": 3000, "block_threads": 1024},
+               {"max_wgs_per_cu": -1}, {"flags": B.RESHARD_XCD_REMAP}, {"flags": B.RESHARD_NO_GATHER}):
+        got, want = run_gpu(shape, dt, sm, ss, dm, ds, rand_bits(shape, dt, 12), **kw)
+        assert_same(got, want)
