@@ -40,11 +40,15 @@ def kernel_hash():
     return h.hexdigest()[:16]
 
 
-def measured_traffic(workload_name):
+def traffic_key(workload_name, flags, strategy):
+    return f"{workload_name}|flags={flags}|{strategy}"
+
+
+def measured_traffic(key):
     """HBM bytes per launch from committed rocprofv3 counter runs, if they match this kernel."""
     try:
         with open(TRAFFIC_FILE) as f:
-            rec = json.load(f).get(workload_name)
+            rec = json.load(f).get(key)
     except (OSError, ValueError):
         return None
     if not rec or rec.get("kernel_hash") != kernel_hash():
@@ -69,7 +73,7 @@ def cpu_baseline(w, src_dev, budget_s):
         out = oracle.reshard(src, w.shape, w.src_mesh, w.src_spec, w.dst_mesh, w.dst_spec)
         times.append(time.perf_counter() - t0)
         del out
-        if time.perf_counter() - t_start >= budget_s or len(times) >= 5:
+        if time.perf_counter() - t_start >= budget_s or len(times) >= 100:
             break
     med = statistics.median(times)
     ncores = len(os.sched_getaffinity(0))
@@ -199,7 +203,14 @@ def main():
             c.copy_(a)
         torch.cuda.synchronize()
         del a, c
-    traffic = measured_traffic(w.name)
+    traffic = measured_traffic(traffic_key(w.name, args.flags, args.strategy))
+    # The dominant kernel: the one that processes most of the plan's chunks
+    # (an execute launches the direct, row-gather and realignment kernels for
+    # the chunks of each kind the plan holds; most workloads use one).
+    n_gather, n_realign = B.reshard_plan_gather_chunks(plan), B.reshard_plan_realign_chunks(plan)
+    n_direct = st["n_descriptors"] - n_gather - n_realign
+    kernel = max((n_direct, "reshard_kernel"), (n_gather, "reshard_gather_kernel"),
+                 (n_realign, "reshard_realign_kernel"))[1]
     out = {
         "metric": METRIC,
         "value": round(gbs, 2),
@@ -221,6 +232,8 @@ def main():
         },
         "pct_of_hbm_peak": round(100.0 * gbs / HBM_PEAK_GBS, 2),
         "roofline": {
+            "kernel": kernel, "launches_per_step": sum(1 for n in (n_direct, n_gather, n_realign) if n)
+                                                        + (args.strategy == "allgather" and n_direct > 0),
             "bound": "hbm", "achieved": round(gbs, 2), "peak": HBM_PEAK_GBS, "unit": "GB/s",
             "frac": round(gbs / HBM_PEAK_GBS, 4), "traffic": traffic,
         },
