@@ -106,7 +106,10 @@ typedef struct {
                                LDS per workgroup; 0 = default (direct chunks: 12 waves per
                                CU; row-gather chunks: 64 / fan-out waves, at least 8; never
                                below 2 workgroups); -1 = no cap */
-    int32_t reserved[4];    /* must be zero */
+    int32_t gather_band;    /* row-gather chunks: column segments per band (>= 0); the chunks
+                               of a row group cover one band of the destination rows after
+                               another; 0 = whole rows (default) */
+    int32_t reserved[3];    /* must be zero */
 } reshard_tuning_t;
 
 /*
@@ -133,8 +136,8 @@ reshard_status_t reshard_plan(int ndim, const int64_t *shape, reshard_dtype_t dt
                               unsigned flags, reshard_plan_t **out);
 
 /* As reshard_plan, with lowering knobs (NULL = defaults).  EINVAL for a bad
- * block size, a negative chunk size, a workgroup cap outside -1, 0, 2..32 or
- * non-zero reserved fields. */
+ * block size, a negative chunk size, a workgroup cap outside -1, 0, 2..32, a
+ * negative band or non-zero reserved fields. */
 reshard_status_t reshard_plan_ex(int ndim, const int64_t *shape, reshard_dtype_t dtype,
                                  int src_mesh_ndim, const int64_t *src_mesh, const char *src_spec,
                                  int dst_mesh_ndim, const int64_t *dst_mesh, const char *dst_spec,

@@ -42,7 +42,8 @@ class ReshardError(RuntimeError):
 
 class reshard_tuning_t(ctypes.Structure):
     _fields_ = [("chunk_bytes", ctypes.c_int64), ("block_threads", ctypes.c_int32),
-                ("max_wgs_per_cu", ctypes.c_int32), ("reserved", ctypes.c_int32 * 4)]
+                ("max_wgs_per_cu", ctypes.c_int32), ("gather_band", ctypes.c_int32),
+                ("reserved", ctypes.c_int32 * 3)]
 
 
 _lib = None
@@ -162,14 +163,14 @@ class Plan:
 
 
 def reshard_plan(shape, dtype, src_mesh, src_spec, dst_mesh, dst_spec, flags=0,
-                 chunk_bytes=0, block_threads=0, max_wgs_per_cu=0):
+                 chunk_bytes=0, block_threads=0, max_wgs_per_cu=0, gather_band=0):
     lib = load()
     h = ctypes.c_void_p()
     args = [len(shape), _i64(shape), _dtype_code(dtype), len(src_mesh), _i64(src_mesh),
             src_spec.encode(), len(dst_mesh), _i64(dst_mesh), dst_spec.encode(), int(flags)]
-    if chunk_bytes or block_threads or max_wgs_per_cu:
+    if chunk_bytes or block_threads or max_wgs_per_cu or gather_band:
         t = reshard_tuning_t(chunk_bytes=int(chunk_bytes), block_threads=int(block_threads),
-                             max_wgs_per_cu=int(max_wgs_per_cu))
+                             max_wgs_per_cu=int(max_wgs_per_cu), gather_band=int(gather_band))
         _check(lib.reshard_plan_ex(*args, ctypes.byref(t), ctypes.byref(h)))
     else:
         _check(lib.reshard_plan(*args, ctypes.byref(h)))

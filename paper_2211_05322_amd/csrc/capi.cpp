@@ -92,6 +92,8 @@ reshard_status_t make_plan(int ndim, const int64_t *shape, reshard_dtype_t dtype
         tn.chunk_bytes = tuning->chunk_bytes;
         if (bt) tn.block_threads = bt;
         tn.max_wgs_per_cu = cap;
+        if (tuning->gather_band < 0) return fail(RESHARD_EINVAL, "tuning.gather_band is negative");
+        tn.gather_band = tuning->gather_band;
     }
     tn.cap_is_default = tn.max_wgs_per_cu == 0;
     if (tn.max_wgs_per_cu == 0) {
@@ -277,8 +279,12 @@ reshard_status_t reshard_debug_execute_host(const reshard_plan_t *plan, void *co
                 const uint32_t dr = i1 * d.ds[0] + i2 * d.ds[1] + i3 * d.ds[2] + 16u * j - d.dst_rel0;
                 const rs::Seg &sg = p->segs[d.pad[0] + g];
                 const uint32_t sr = i1 * sg.ss[0] + i2 * sg.ss[1] + i3 * sg.ss[2] + 16u * jj;
+                if (sg.src_base + sr + 16 > uint64_t(p->src_local_numel[sg.buf] * p->es))
+                    return fail(RESHARD_EINVAL, "internal: gather load outside its source shard");
                 const char *src = static_cast<const char *>(src_ptrs[sg.buf]) + sg.src_base + sr;
                 for (uint32_t r = 0; r < d.nfan; ++r) {
+                    if (d.dst_base + dr + 16 > uint64_t(p->dst_local_numel[p->fan[d.fan_off + r]] * p->es))
+                        return fail(RESHARD_EINVAL, "internal: gather store outside its destination shard");
                     char *dst = static_cast<char *>(dst_ptrs[p->fan[d.fan_off + r]]) + d.dst_base + dr;
                     std::memcpy(dst, src, 16);
                 }

@@ -542,36 +542,51 @@ bool lower_gather_group(Plan &p, const std::vector<size_t> &group, int64_t chunk
     d.kind = uint8_t(make_kind(4, uint32_t(levels)));
     d.nfan = uint16_t(nfan);
     d.fan_off = uint32_t(fan_off);
-    d.pad[0] = uint32_t(p.segs.size());
-    d.pad[1] = uint32_t(ns);
-    // destination offset of slot v of the group (64-bit), levels innermost first
-    auto dst_off = [&](uint64_t v) {
-        uint64_t row = v / spr, off = dso + (v - row * spr) * 16;
-        for (size_t i = 0; i < lv.size(); ++i) {
-            const uint64_t n = uint64_t(lv[i].n);
-            const uint64_t idx = i + 1 == lv.size() ? row : row % n;
-            off += idx * uint64_t(lv[i].ds);
-            row = i + 1 == lv.size() ? 0 : row / n;
-        }
-        return off;
-    };
-    uint64_t cv = uint64_t(std::max<int64_t>(16, chunk_bytes / 16)) / 16 * 16;
-    const uint64_t total = rows * spr;
-    if (p.descs.size() + out.size() + (total + cv - 1) / cv > kMaxDescs) {
+    // Column bands of `band` segments, one after another; each band's chunks
+    // are ranges of its slots over consecutive rows.
+    const uint64_t band = p.tuning.gather_band > 0 && uint64_t(p.tuning.gather_band) < ns
+                              ? uint64_t(p.tuning.gather_band) : uint64_t(ns);
+    const uint64_t cv = uint64_t(std::max<int64_t>(16, chunk_bytes / 16)) / 16 * 16;
+    uint64_t nchunks = 0;
+    for (uint64_t b0 = 0; b0 < ns; b0 += band)
+        nchunks += (rows * std::min<uint64_t>(band, ns - b0) * sps + cv - 1) / cv;
+    if (p.descs.size() + out.size() + nchunks > kMaxDescs) {
         p.too_many = true;
         return false;
     }
     std::vector<Desc> mine;
-    for (uint64_t v0 = 0; v0 < total;) {
-        uint64_t v1 = std::min(total, v0 + cv);
-        const uint64_t first = dst_off(v0);
-        while (dst_off(v1 - 1) + 16 - first >= kMaxChunkSpan) v1 = v0 + (v1 - v0) / 2;
-        d.v0 = uint32_t(v0);
-        d.v1 = uint32_t(v1);
-        d.dst_base = first;
-        d.dst_rel0 = uint32_t(first - dso);
-        mine.push_back(d);
-        v0 = v1;
+    for (uint64_t b0 = 0; b0 < ns; b0 += band) {
+        const uint64_t nb = std::min<uint64_t>(band, ns - b0), bw = nb * sps;
+        const uint64_t bso = dso + b0 * sps * 16;  // destination offset of the band's first slot
+        const FastDiv fb = make_fastdiv(uint32_t(bw));
+        d.vpr = uint32_t(bw);
+        d.mul_vpr = fb.mul;
+        d.sh_vpr = uint8_t(fb.shift);
+        d.pad[0] = uint32_t(p.segs.size() + b0);
+        d.pad[1] = uint32_t(nb);
+        // destination offset of slot v of the band (64-bit), levels innermost first
+        auto dst_off = [&](uint64_t v) {
+            uint64_t row = v / bw, off = bso + (v - row * bw) * 16;
+            for (size_t i = 0; i < lv.size(); ++i) {
+                const uint64_t n = uint64_t(lv[i].n);
+                const uint64_t idx = i + 1 == lv.size() ? row : row % n;
+                off += idx * uint64_t(lv[i].ds);
+                row = i + 1 == lv.size() ? 0 : row / n;
+            }
+            return off;
+        };
+        const uint64_t total = rows * bw;
+        for (uint64_t v0 = 0; v0 < total;) {
+            uint64_t v1 = std::min(total, v0 + cv);
+            const uint64_t first = dst_off(v0);
+            while (dst_off(v1 - 1) + 16 - first >= kMaxChunkSpan) v1 = v0 + (v1 - v0) / 2;
+            d.v0 = uint32_t(v0);
+            d.v1 = uint32_t(v1);
+            d.dst_base = first;
+            d.dst_rel0 = uint32_t(first - bso);
+            mine.push_back(d);
+            v0 = v1;
+        }
     }
     p.segs.insert(p.segs.end(), seg.begin(), seg.end());
     out.insert(out.end(), mine.begin(), mine.end());

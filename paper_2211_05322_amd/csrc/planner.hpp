@@ -47,6 +47,7 @@ struct Tuning {
     int32_t block_threads = 256;
     int32_t max_wgs_per_cu = 0;  // resolved cap (0: none)
     bool cap_is_default = true;  // the caller left the cap to the library
+    int32_t gather_band = 0;     // row gather: segments per column band (0: whole rows)
 };
 
 struct Plan {

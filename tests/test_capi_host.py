@@ -341,14 +341,30 @@ GATHER_CASES = [
 
 @pytest.mark.parametrize("case", GATHER_CASES)
 @pytest.mark.parametrize("chunk", [0, 256, 3000])
-def test_host_gather(case, chunk):
+@pytest.mark.parametrize("band", [0, 1, 3])
+def test_host_gather(case, chunk, band):
     shape, dt, sm, ss, dm, ds = case
-    p = plan_of(shape, dt, sm, ss, dm, ds, chunk_bytes=chunk)
+    p = plan_of(shape, dt, sm, ss, dm, ds, chunk_bytes=chunk, gather_band=band)
     assert B.reshard_plan_gather_chunks(p) > 0, "case should take the row-gather path"
-    host_case(shape, dt, sm, ss, dm, ds, chunk_bytes=chunk)
+    host_case(shape, dt, sm, ss, dm, ds, chunk_bytes=chunk, gather_band=band)
     q = plan_of(shape, dt, sm, ss, dm, ds, flags=B.RESHARD_NO_GATHER)
     assert B.reshard_plan_gather_chunks(q) == 0
     host_case(shape, dt, sm, ss, dm, ds, flags=B.RESHARD_NO_GATHER)
+
+
+def test_gather_band_chunk_count():
+    # bands tile the rows: same slots in total, each band's chunks separate
+    shape, dt, sm, ss, dm, ds = GATHER_CASES[4]
+    es = 2
+    row_slots = shape[2] * es // 16
+    rows = shape[0] * shape[1] // 8
+    for band, cb in ((0, 4096), (1, 4096), (4, 4096), (5, 1024), (32, 4096), (40, 4096)):
+        p = plan_of(shape, dt, sm, ss, dm, ds, chunk_bytes=cb, gather_band=band)
+        nseg = 32
+        b = band if 0 < band < nseg else nseg
+        per_row = [min(b, nseg - b0) * row_slots // nseg for b0 in range(0, nseg, b)]
+        want = 8 * sum(-(-rows * w // (cb // 16)) for w in per_row)
+        assert B.reshard_plan_gather_chunks(p) == want, band
 
 
 def test_gather_used_by_column_split_workloads():

@@ -308,6 +308,7 @@ def test_gather_path(case):
     _say(f"gather {case}")
     assert B.reshard_plan_gather_chunks(B.reshard_plan(shape, dt, sm, ss, dm, ds)) > 0
     for kw in ({}, {"chunk_bytes": 256, "block_threads": 64}, {"chunk_bytes": 3000, "block_threads": 1024},
-               {"max_wgs_per_cu": -1}, {"flags": B.RESHARD_XCD_REMAP}, {"flags": B.RESHARD_NO_GATHER}):
+               {"max_wgs_per_cu": -1}, {"flags": B.RESHARD_XCD_REMAP}, {"flags": B.RESHARD_NO_GATHER},
+               {"gather_band": 1}, {"gather_band": 3, "chunk_bytes": 1024}):
         got, want = run_gpu(shape, dt, sm, ss, dm, ds, rand_bits(shape, dt, 12), **kw)
         assert_same(got, want)
