@@ -3,10 +3,13 @@
 
 One step = one reshard_execute of the whole resharding task (one fused
 kernel launch reading every unique slice once and writing every destination
-shard, replicas included) over inputs already resident in HBM.  The plan
-(decomposition, sender choice, lowering) is built once before the timed
-region, as a resharding task is planned once and repeated every iteration.
-Its cost is reported separately as plan_us.
+shard, replicas included) over inputs already resident in HBM.  Consecutive
+steps use distinct sets of source and destination buffers in turn (at least
+4 GiB of buffers in all), so no step finds its inputs in the 256 MB
+last-level cache from the steps just before it.  The plan (decomposition,
+sender choice, lowering) is built once before the timed region, as a
+resharding task is planned once and repeated every iteration.  Its cost is
+reported separately as plan_us.
 
 Prints ONE JSON line.  Default workload: fp16 [8,2048,12288] (403 MB), source
 mesh (4,8) "R R S^{01}" -> destination mesh (4,8) "R S^1 R" (4x replicated),
@@ -96,6 +99,9 @@ def main():
     ap.add_argument("--chunk-bytes", type=int, default=0)
     ap.add_argument("--block-threads", type=int, default=0)
     ap.add_argument("--flags", type=int, default=0)
+    ap.add_argument("--buffer-sets", type=int, default=0,
+                    help="distinct source/destination buffer sets used in turn (0: enough for 4 GiB; "
+                         "1: the same buffers every step)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-budget", type=float, default=10.0, help="seconds of oracle timing")
     ap.add_argument("--no-context", action="store_true", help="skip the device copy/fill ceiling")
@@ -141,31 +147,41 @@ def main():
     plan_us = (time.perf_counter() - t0) * 1e6
     st = B.reshard_plan_stats(plan)
     dst = B.empty_shards(plan, 1)
+    footprint = sum(t.numel() * t.element_size() for t in src + dst)
+    nsets = args.buffer_sets or min(64, max(2, -(-(4 << 30) // max(footprint, 1))))
+    sets = [(src, dst)]
+    for _ in range(nsets - 1):
+        s2 = B.empty_shards(scatter, 1)
+        B.reshard_execute(scatter, [x], s2)
+        sets.append((s2, B.empty_shards(plan, 1)))
     torch.cuda.synchronize()
 
-    for _ in range(args.warmup):
-        B.reshard_execute(plan, src, dst, stream=stream)
+    for k in range(args.warmup):
+        B.reshard_execute(plan, *sets[k % nsets], stream=stream)
     torch.cuda.synchronize()
 
     ev0 = torch.cuda.Event(enable_timing=True)
     ev1 = torch.cuda.Event(enable_timing=True)
     h0 = time.perf_counter()
     ev0.record(stream)
-    for _ in range(args.steps):
-        B.reshard_execute(plan, src, dst, stream=stream)
+    for k in range(args.steps):
+        B.reshard_execute(plan, *sets[k % nsets], stream=stream)
     ev1.record(stream)
     host_us = (time.perf_counter() - h0) * 1e6 / args.steps
     torch.cuda.synchronize()
     ms_total = ev0.elapsed_time(ev1)
     ms_per_step = ms_total / args.steps
 
-    # Round-trip check through the library: dst -> one buffer must equal x.
+    # Round-trip check through the library: every set's dst -> one buffer
+    # must equal x.
     back_plan = B.reshard_plan(w.shape, w.dtype, w.dst_mesh, w.dst_spec, (1,), rep, block_threads=1024)
     back = B.empty_shards(back_plan, 1)
-    B.reshard_execute(back_plan, dst, back)
-    torch.cuda.synchronize()
-    roundtrip_ok = bool(torch.equal(back[0].view(torch.uint8), x.view(torch.uint8)))
-    del back
+    roundtrip_ok = True
+    for _, d_ in sets:
+        B.reshard_execute(back_plan, d_, back)
+        torch.cuda.synchronize()
+        roundtrip_ok &= bool(torch.equal(back[0].view(torch.uint8), x.view(torch.uint8)))
+    del back, sets, dst
 
     nbytes = st["bytes_read"] + st["bytes_written"]
     gbs = nbytes / (ms_per_step * 1e-3) / 1e9
@@ -229,6 +245,7 @@ def main():
             "dst_mesh": list(w.dst_mesh), "dst_spec": w.dst_spec, "bytes_read": st["bytes_read"],
             "bytes_written": st["bytes_written"], "unit_tasks": st["n_unit_tasks"],
             "workgroups": st["n_descriptors"], "max_fanout": st["max_fanout"], "strategy": args.strategy,
+            "buffer_sets": nsets,
         },
         "pct_of_hbm_peak": round(100.0 * gbs / HBM_PEAK_GBS, 2),
         "roofline": {
