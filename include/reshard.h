@@ -103,9 +103,10 @@ typedef struct {
                                so a large plan has >= 4096 chunks); whole vectors */
     int32_t block_threads;  /* threads per workgroup: 64, 128, 256, 512 or 1024 (default 256) */
     int32_t max_wgs_per_cu; /* cap on resident workgroups per CU, 2..32, enforced by reserving
-                               LDS per workgroup; 0 = default (direct chunks: 12 waves per
-                               CU; row-gather chunks: 64 / fan-out waves, at least 8; never
-                               below 2 workgroups); -1 = no cap */
+                               LDS per workgroup; 0 = default, chosen per kernel from its
+                               fan-out (direct chunks: 16 waves per CU at fan-out <= 2, 12
+                               above; row-gather chunks: 64 / fan-out waves, at least 8;
+                               never below 2 workgroups); -1 = no cap */
     int32_t gather_band;    /* row-gather chunks: column segments per band (>= 0); the chunks
                                of a row group cover one band of the destination rows after
                                another; 0 = whole rows (default) */

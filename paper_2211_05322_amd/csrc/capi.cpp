@@ -95,15 +95,10 @@ reshard_status_t make_plan(int ndim, const int64_t *shape, reshard_dtype_t dtype
         if (tuning->gather_band < 0) return fail(RESHARD_EINVAL, "tuning.gather_band is negative");
         tn.gather_band = tuning->gather_band;
     }
+    // 0: the library picks each kernel's residency at launch from its
+    // fan-out; -1: no cap
     tn.cap_is_default = tn.max_wgs_per_cu == 0;
-    if (tn.max_wgs_per_cu == 0) {
-        // default residency: about 12 waves per CU (fewer concurrent write
-        // streams schedule better in HBM), never below 2 workgroups
-        const int waves = tn.block_threads / 64;
-        tn.max_wgs_per_cu = std::max(2, 12 / waves);
-    } else if (tn.max_wgs_per_cu == -1) {
-        tn.max_wgs_per_cu = 0;
-    }
+    if (tn.max_wgs_per_cu == -1) tn.max_wgs_per_cu = 0;
     int64_t ns = 0, nd = 0;
     reshard_status_t st = check_mesh("source", smn, sm, ns);
     if (st != RESHARD_OK) return st;

@@ -652,6 +652,15 @@ reshard_status_t launch_one(K kernel, A a, uint32_t ndesc, bool remap, uint32_t 
     return RESHARD_OK;
 }
 
+// LDS reservation (unused by the direct kernel; the gather kernel's segment
+// table fits inside it) that caps resident workgroups per CU at about
+// `waves` waves, never below 2 workgroups: the CU holds 160 KiB of LDS.
+uint32_t residency_lds(uint32_t waves, uint32_t block) {
+    uint32_t wgs = waves / (block / 64u ? block / 64u : 1u);
+    if (wgs < 2u) wgs = 2u;
+    return wgs >= 32u ? 0u : (160u * 1024u / wgs) & ~1023u;
+}
+
 template <int NPTR>
 reshard_status_t launch(const Plan &p, const Desc *descs, const int32_t *fan, const Seg *segs,
                         void *const *src_ptrs, void *const *dst_ptrs, hipStream_t stream) {
@@ -667,10 +676,15 @@ reshard_status_t launch(const Plan &p, const Desc *descs, const int32_t *fan, co
     for (int64_t k = 0; k < p.dst.ndev; ++k) a.ptr[p.src.ndev + k] = dst_ptrs[k];
     const bool remap = (p.flags & RESHARD_XCD_REMAP) != 0;
     const uint32_t block = uint32_t(p.tuning.block_threads);
-    // An LDS reservation (unused by the direct kernel) caps resident
-    // workgroups per CU: the CU holds 160 KiB of LDS.
-    const uint32_t cap_lds =
+    // Residency cap of the direct and gather kernels: the caller's, else
+    // chosen from the kernel's fan-out (measured with buffers that are not
+    // cache-resident): direct chunks 16 waves per CU at fan-out <= 2, 12
+    // above; gather chunks about 64 receiver write streams per CU (64 /
+    // fan-out waves, at least 8).
+    const uint32_t user_lds =
         p.tuning.max_wgs_per_cu ? (160u * 1024u / uint32_t(p.tuning.max_wgs_per_cu)) & ~1023u : 0u;
+    const uint32_t cap_lds =
+        p.tuning.cap_is_default ? residency_lds(p.direct_fanout <= 2 ? 16u : 12u, block) : user_lds;
     const uint32_t n_direct = uint32_t(p.n_direct), n_gather = uint32_t(p.n_gather);
     const uint32_t n_realign = uint32_t(p.descs.size() - p.n_direct - p.n_gather);
     const uint32_t n_phase1 = uint32_t(p.n_phase1);
@@ -685,18 +699,10 @@ reshard_status_t launch(const Plan &p, const Desc *descs, const int32_t *fan, co
         if (st != RESHARD_OK) return st;
     }
     if (n_gather) {
-        // Default residency for the gather kernel: about 64 receiver write
-        // streams per CU (64 / fan-out waves, at least 8 waves) -- measured
-        // best at fan-out 4 and 8.  The segment entries it stages in LDS fit
-        // inside that reservation.
-        uint32_t gcap_lds = cap_lds;
+        uint32_t gcap_lds = user_lds;
         if (p.tuning.cap_is_default) {
             const uint32_t fan = uint32_t(p.gather_fanout > 0 ? p.gather_fanout : 1);
-            uint32_t waves = 64u / fan;
-            if (waves < 8u) waves = 8u;
-            uint32_t wgs = waves / (block / 64u ? block / 64u : 1u);
-            if (wgs < 2u) wgs = 2u;
-            gcap_lds = wgs >= 32u ? 0u : (160u * 1024u / wgs) & ~1023u;
+            gcap_lds = residency_lds(64u / fan > 8u ? 64u / fan : 8u, block);
         }
         const uint32_t need = (12u + 8u) * kMaxSegs;
         const uint32_t glds = gcap_lds > need ? gcap_lds : need;

@@ -780,6 +780,8 @@ void lower(Plan &p) {
         for (const auto &t : p.tasks)
             p.bytes_read += t.bytes * (p.dst.shard_devs_off[t.dst_shard + 1] - p.dst.shard_devs_off[t.dst_shard]);
     }
+    p.direct_fanout = 0;
+    for (size_t i = 0; i < p.n_direct; ++i) p.direct_fanout = std::max<int64_t>(p.direct_fanout, p.descs[i].nfan);
     p.bytes_written = 0;
     p.dst_local_numel.assign(p.dst.ndev, 0);
     p.src_local_numel.assign(p.src.ndev, 0);

@@ -45,8 +45,8 @@ struct UnitTask {
 struct Tuning {
     int64_t chunk_bytes = 0;   // 0: automatic
     int32_t block_threads = 256;
-    int32_t max_wgs_per_cu = 0;  // resolved cap (0: none)
-    bool cap_is_default = true;  // the caller left the cap to the library
+    int32_t max_wgs_per_cu = 0;  // the caller's cap (0: none)
+    bool cap_is_default = true;  // the caller left the cap to the library (chosen at launch)
     int32_t gather_band = 0;     // row gather: segments per column band (0: whole rows)
 };
 
@@ -69,6 +69,7 @@ struct Plan {
                                // the rest: realignment chunks
     std::vector<Seg> segs;     // row-gather segment entries
     int64_t gather_fanout = 0; // largest receiver count among row-gather chunks
+    int64_t direct_fanout = 0; // largest receiver count among direct chunks
     size_t n_phase1 = 0;       // descs[0, n_phase1) run before descs[n_phase1, n_direct)
                                // (two launches; only the all-gather strategy has a second phase)
     std::vector<int64_t> src_local_numel, dst_local_numel;  // per device
