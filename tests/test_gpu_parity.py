@@ -312,3 +312,64 @@ def test_gather_path(case):
                {"gather_band": 1}, {"gather_band": 3, "chunk_bytes": 1024}):
         got, want = run_gpu(shape, dt, sm, ss, dm, ds, rand_bits(shape, dt, 12), **kw)
         assert_same(got, want)
+
+
+# ------------------------------------------------------------ maximum sizes
+
+def test_max_buffers_direct_and_gather():
+    """496 buffers (the compiled limit): the large kernel-argument block, on
+    the direct path (fan-out 2) and on the row-gather path (248 senders per
+    destination row)."""
+    for case in (((496, 248), "float32", (248,), "S^0R", (2, 124), "RS^1"),
+                 ((248, 992), "float32", (248,), "RS^0", (2, 124), "S^1R")):
+        shape, dt, sm, ss, dm, ds = case
+        _say(f"max buffers {case}")
+        p = B.reshard_plan(shape, dt, sm, ss, dm, ds)
+        assert p.n_src + p.n_dst == 496
+        if ss == "RS^0":
+            assert B.reshard_plan_gather_chunks(p) > 0
+        got, want = run_gpu(shape, dt, sm, ss, dm, ds, rand_bits(shape, dt, 21))
+        assert_same(got, want)
+
+
+def _check_against_boxes(x, dst, shape, mesh, spec):
+    """Destination k must equal x sliced at the oracle's box of device k."""
+    dims = oracle.parse_spec(spec, len(shape), len(mesh))
+    for k, d in enumerate(dst):
+        box = oracle.device_box(shape, mesh, dims, k)
+        want = x[tuple(slice(lo, hi) for lo, hi in box)]
+        assert tuple(d.shape) == tuple(want.shape)
+        assert torch.equal(d.view(torch.int16), want.view(torch.int16)), f"destination {k} differs"
+
+
+@pytest.mark.parametrize("case", [
+    # one 5 GiB source to two 5 GiB replicas (offsets past 2^32 on both sides)
+    ((5, 1 << 29), (1,), "RR", (2,), "RR"),
+    # two senders' 512 MiB column halves gathered into 1 GiB rows of one 5 GiB buffer
+    ((5, 1 << 29), (2,), "RS^0", (1,), "RR"),
+    # rows of 2^30 + 10 bytes split unevenly: different 16-byte phases, 5 GiB source
+    ((5, (1 << 29) + 5), (1,), "RR", (2,), "RS^0"),
+])
+def test_over_4gib(case):
+    """Buffers above 4 GiB: every destination compared, element by element on
+    the GPU, with the tensor sliced at the oracle's shard boxes."""
+    shape, sm, ss, dm, ds = case
+    _say(f"over 4 GiB {case}")
+    x = make_workload_tensor(WORKLOADS[5].__class__("big", shape, "float16", "bits", sm, ss, dm, ds),
+                             seed=3, device="cuda")
+    dims = oracle.parse_spec(ss, len(shape), len(sm))
+    src = []
+    for k in range(int(np.prod(sm))):
+        box = oracle.device_box(shape, sm, dims, k)
+        src.append(x[tuple(slice(lo, hi) for lo, hi in box)].contiguous())
+    p = B.reshard_plan(shape, "float16", sm, ss, dm, ds)
+    dst = B.empty_shards(p, 1)
+    for d in dst:
+        d.view(torch.int16).fill_(-1)
+    B.reshard_execute(p, src, dst)
+    torch.cuda.synchronize()
+    del src
+    _check_against_boxes(x, dst, shape, dm, ds)
+    _say(f"over 4 GiB {case} ok")
+    del x, dst
+    torch.cuda.empty_cache()
