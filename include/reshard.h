@@ -201,9 +201,16 @@ int64_t reshard_plan_lds_bytes(const reshard_plan_t *plan);
 int64_t reshard_plan_realign_chunks(const reshard_plan_t *plan);
 
 /* Number of workgroup chunks that write whole destination rows gathered
- * from several senders (RESHARD_NO_GATHER turns them off), or -1 for a NULL
- * plan. */
+ * from several senders whose row segments are equal and 16-byte aligned
+ * (RESHARD_NO_GATHER turns them off), or -1 for a NULL plan. */
 int64_t reshard_plan_gather_chunks(const reshard_plan_t *plan);
+
+/* Number of workgroup chunks that write 16-byte slots of contiguous
+ * destination rows gathered from several senders whose row segments have
+ * any widths of at least 16 bytes and any byte alignment (uneven splits,
+ * rows in different 16-byte phases; RESHARD_NO_GATHER turns them off), or
+ * -1 for a NULL plan. */
+int64_t reshard_plan_unaligned_gather_chunks(const reshard_plan_t *plan);
 
 /*
  * Unit task `index` (0 <= index < n_unit_tasks), in lexicographic order of the

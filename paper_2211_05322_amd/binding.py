@@ -82,6 +82,8 @@ def load(path=None):
     lib.reshard_plan_gather_chunks.restype = ctypes.c_int64
     lib.reshard_plan_realign_chunks.argtypes = [ctypes.c_void_p]
     lib.reshard_plan_realign_chunks.restype = ctypes.c_int64
+    lib.reshard_plan_unaligned_gather_chunks.argtypes = [ctypes.c_void_p]
+    lib.reshard_plan_unaligned_gather_chunks.restype = ctypes.c_int64
     lib.reshard_plan_unit_task.argtypes = [ctypes.c_void_p, ctypes.c_int64, _I64P, _I64P, _I64P,
                                            _I64P, ctypes.c_int64, _I64P, _I64P, ctypes.c_int64, _I64P]
     lib.reshard_plan_unit_task.restype = ctypes.c_int
@@ -235,6 +237,10 @@ def reshard_plan_gather_chunks(plan):
 
 def reshard_plan_realign_chunks(plan):
     return int(load().reshard_plan_realign_chunks(plan.handle))
+
+
+def reshard_plan_unaligned_gather_chunks(plan):
+    return int(load().reshard_plan_unaligned_gather_chunks(plan.handle))
 
 
 def reshard_plan_unit_task(plan, index):

@@ -216,7 +216,12 @@ int64_t reshard_plan_gather_chunks(const reshard_plan_t *plan) {
 
 int64_t reshard_plan_realign_chunks(const reshard_plan_t *plan) {
     const rs::Plan *p = as_plan(plan);
-    return p ? int64_t(p->descs.size() - p->n_direct - p->n_gather) : -1;
+    return p ? int64_t(p->descs.size() - p->n_direct - p->n_gather - p->n_gather_u) : -1;
+}
+
+int64_t reshard_plan_unaligned_gather_chunks(const reshard_plan_t *plan) {
+    const rs::Plan *p = as_plan(plan);
+    return p ? int64_t(p->n_gather_u) : -1;
 }
 
 reshard_status_t reshard_plan_unit_task(const reshard_plan_t *plan, int64_t index, int64_t *lo, int64_t *hi,
@@ -259,6 +264,67 @@ reshard_status_t reshard_debug_execute_host(const reshard_plan_t *plan, void *co
         const rs::Desc &d = p->descs[di];
         const uint32_t w = 1u << rs::kind_log2w(d.kind);
         const uint32_t levels = rs::kind_levels(d.kind);
+        if (di >= p->n_direct + p->n_gather && di < p->n_direct + p->n_gather + p->n_gather_u) {
+            // unaligned row-gather chunk: the kernel's slot -> pieces arithmetic
+            const uint32_t rb = d.vpr, ns = d.pad[1];
+            if (d.pad[0] + ns > p->segs.size() || ns == 0) return fail(RESHARD_EINVAL, "internal: segment table range");
+            const rs::Seg *sg = &p->segs[d.pad[0]];
+            if (sg[0].col != 0) return fail(RESHARD_EINVAL, "internal: first segment does not start the row");
+            auto find_segment = [&](uint32_t col) {
+                uint32_t g = rs::fastdiv(col, d.batch, d.pad[2]);
+                if (g >= ns) g = ns - 1;
+                while (g > 0 && col < sg[g].col) --g;
+                while (g + 1 < ns && col >= sg[g + 1].col) ++g;
+                return g;
+            };
+            // copy piece [col, col + len) of segment g, row `row`, to out
+            auto piece = [&](uint32_t row, uint32_t g, uint32_t col, uint32_t len, uint8_t *out) -> bool {
+                const uint32_t send = g + 1 < ns ? sg[g + 1].col : rb;
+                if (col < sg[g].col || col + len > send) return false;
+                uint32_t i1 = 0, i2 = 0, i3 = 0;
+                if (levels == 1) rs::row_indices<1>(d, row, i1, i2, i3);
+                else if (levels == 2) rs::row_indices<2>(d, row, i1, i2, i3);
+                else rs::row_indices<3>(d, row, i1, i2, i3);
+                const uint32_t off = i1 * sg[g].ss[0] + i2 * sg[g].ss[1] + i3 * sg[g].ss[2] + (col - sg[g].col);
+                const uint64_t q = sg[g].src_base + off;
+                if (q + len > uint64_t(p->src_local_numel[sg[g].buf] * p->es)) return false;
+                std::memcpy(out, static_cast<const char *>(src_ptrs[sg[g].buf]) + q, len);
+                return true;
+            };
+            for (uint32_t ls = d.v0; ls < d.v1; ++ls) {
+                const uint32_t c0 = 16u * ls;
+                const uint32_t lo = std::max(c0, d.ss[2]), hi = std::min(c0 + 16u, d.src_rel0);
+                if (lo >= hi) continue;
+                uint8_t out[16];
+                const uint32_t t = lo + d.ss[1];
+                const uint32_t dr = rs::fastdiv(t, d.mul_vpr, d.sh_vpr);
+                uint32_t row = d.ss[0] + dr, col = t - dr * rb;
+                uint32_t g = find_segment(col);
+                const uint32_t send = g + 1 < ns ? sg[g + 1].col : rb;
+                const uint32_t e1 = lo + std::min(hi - lo, send - col);
+                if (!piece(row, g, col, e1 - lo, out + (lo - c0)))
+                    return fail(RESHARD_EINVAL, "internal: unaligned gather piece outside its segment or shard");
+                if (e1 < hi) {
+                    if (send == rb) {
+                        ++row;
+                        col = 0;
+                        g = 0;
+                    } else {
+                        col = send;
+                        ++g;
+                    }
+                    if (!piece(row, g, col, hi - e1, out + (e1 - c0)))
+                        return fail(RESHARD_EINVAL, "internal: unaligned gather piece outside its segment or shard");
+                }
+                for (uint32_t r = 0; r < d.nfan; ++r) {
+                    const int32_t dev = p->fan[d.fan_off + r];
+                    if (d.dst_base + hi > uint64_t(p->dst_local_numel[dev] * p->es))
+                        return fail(RESHARD_EINVAL, "internal: unaligned gather store outside its destination shard");
+                    std::memcpy(static_cast<char *>(dst_ptrs[dev]) + d.dst_base + lo, out + (lo - c0), hi - lo);
+                }
+            }
+            continue;
+        }
         if (di >= p->n_direct && di < p->n_direct + p->n_gather) {
             // row-gather chunk: the kernel's slot -> (row, segment) arithmetic
             const uint32_t spr = d.vpr, sps = d.run;

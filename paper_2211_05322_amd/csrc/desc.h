@@ -104,12 +104,30 @@ static_assert(sizeof(Desc) == 112, "descriptor layout is shared by host and devi
 // the 64-bit offset of the group's first row at the segment's first column,
 // and the sender's strides of the outer levels (mod 2^32).  Source offsets
 // are relative to that origin and below 2^32.
+//
+// Unaligned row gather (own section and kernel).  For row groups whose
+// segments tile the destination row in any widths of at least 16 bytes and
+// whose destination rows are contiguous, the chunks cover 16-byte slots of
+// the destination buffer itself (buffer-aligned, so a slot may hold the end
+// of one segment or row and the start of the next: at most two pieces).
+// Fields: v1 = slots in the chunk (v0 = 0), dst_base = byte offset of its
+// first slot; vpr = row bytes with mul_vpr/sh_vpr; n1, n2 and their
+// multipliers = the source levels; ss[0] = row0 and ss[1] = cofs0 (int32):
+// chunk byte c lies at row row0 + (c + cofs0) / vpr, column (c + cofs0) mod
+// vpr; ss[2] = reg_lo, src_rel0 = reg_hi: the chunk bytes [reg_lo, reg_hi)
+// belong to the group; run = nominal segment width (vpr / segments, a first
+// guess for the segment of a column) with batch/pad[2] its fast division;
+// pad[0], pad[1] the segment entries.  Each entry's `col` is its first byte
+// within the row; its src_base is the source offset of the group's first row
+// at that column (any byte alignment).
 struct Seg {
     uint64_t src_base;
     uint32_t ss[3];
     uint32_t buf;
+    uint32_t col;  // unaligned gather: first byte of the segment within the row
+    uint32_t pad;
 };
-static_assert(sizeof(Seg) == 24, "segment entries are shared by host and device");
+static_assert(sizeof(Seg) == 32, "segment entries are shared by host and device");
 constexpr uint32_t kMaxSegs = 256;  // segment entries one gather chunk may stage
 
 // Outer-level indices of a row (level 1 = innermost outer level).

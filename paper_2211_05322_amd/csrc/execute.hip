@@ -560,6 +560,168 @@ __global__ __launch_bounds__(1024) void reshard_gather_kernel(KArgs<NPTR> args) 
     run_gather_levels(d, a);
 }
 
+// Unaligned row gather (see desc.h): a workgroup writes 16-byte slots of the
+// receivers' buffers; each slot holds at most two pieces (end of a segment or
+// row, start of the next), each read as the aligned source word(s) holding
+// it and funnel-shifted into place.  A word is loaded only if it holds a
+// byte of its piece, so no load leaves the 4 KiB page of a byte it needs.
+// LDS: 64-bit source pointers at 0, three strides per segment at
+// 8 * kMaxSegs, segment starts (bytes within the row) at 20 * kMaxSegs.
+constexpr uint32_t kGatherULds = 24u * kMaxSegs;
+
+template <int NPTR>
+__device__ __forceinline__ void stage_segments_u(const Desc &d, const RS_CONST KArgs<NPTR> *a) {
+    uint64_t *sp = reinterpret_cast<uint64_t *>(rs_lds);
+    uint32_t *sst = reinterpret_cast<uint32_t *>(rs_lds + 8u * kMaxSegs);
+    uint32_t *scol = reinterpret_cast<uint32_t *>(rs_lds + 20u * kMaxSegs);
+    const RS_CONST Seg *segs = (const RS_CONST Seg *)(a->segs + d.pad[0]);
+    for (uint32_t g = threadIdx.x; g < d.pad[1]; g += blockDim.x) {
+        sp[g] = uint64_t(a->ptr[segs[g].buf]) + segs[g].src_base;
+        sst[3 * g] = segs[g].ss[0];
+        sst[3 * g + 1] = segs[g].ss[1];
+        sst[3 * g + 2] = segs[g].ss[2];
+        scol[g] = segs[g].col;
+    }
+}
+
+// Segment holding row byte `col`: a guess from the nominal width, then the
+// staged segment starts decide.
+__device__ __forceinline__ uint32_t find_segment(const Desc &d, const uint32_t *scol, uint32_t col) {
+    const uint32_t ns = d.pad[1];
+    uint32_t g = fastdiv(col, d.batch, d.pad[2]);
+    if (g >= ns) g = ns - 1;
+    while (g > 0 && col < scol[g]) --g;
+    while (g + 1 < ns && col >= scol[g + 1]) ++g;
+    return g;
+}
+
+template <int L>
+__device__ __forceinline__ uint64_t segment_addr(const Desc &d, const uint64_t *sp, const uint32_t *sst,
+                                                 const uint32_t *scol, uint32_t g, uint32_t row, uint32_t col) {
+    uint32_t i1, i2, i3;
+    row_indices<L>(d, row, i1, i2, i3);
+    const uint32_t off = i1 * sst[3 * g] + i2 * sst[3 * g + 1] + i3 * sst[3 * g + 2] + (col - scol[g]);
+    return sp[g] + off;
+}
+
+struct USlot {
+    u32x4 a0, a1, b0, b1;   // aligned source words of the two pieces
+    uint32_t lo, hi, e1;    // slot bytes [lo, hi) in chunk coordinates; piece 2 starts at e1
+    uint32_t sha, shb;      // byte offsets of the pieces in their first words
+};
+
+template <int L>
+__device__ __forceinline__ void uslot_load(const Desc &d, const uint64_t *sp, const uint32_t *sst,
+                                           const uint32_t *scol, uint32_t c0, USlot &s) {
+    const u32x4 z = {0u, 0u, 0u, 0u};
+    s.a1 = z;
+    s.b1 = z;
+    s.lo = c0 > d.ss[2] ? c0 : d.ss[2];
+    s.hi = c0 + 16u < d.src_rel0 ? c0 + 16u : d.src_rel0;
+    s.e1 = s.hi;
+    s.sha = 0;
+    s.shb = 0;
+    if (s.lo >= s.hi) return;
+    const uint32_t rb = d.vpr, ns = d.pad[1];
+    const uint32_t t = s.lo + d.ss[1];  // >= 0: the region starts at ss[2] = -cofs0 in the first chunk
+    const uint32_t dr = fastdiv(t, d.mul_vpr, d.sh_vpr);
+    uint32_t row = d.ss[0] + dr, col = t - dr * rb;
+    uint32_t g = find_segment(d, scol, col);
+    const uint32_t send = g + 1 < ns ? scol[g + 1] : rb;
+    s.e1 = s.lo + ((s.hi - s.lo) < (send - col) ? (s.hi - s.lo) : (send - col));
+    uint64_t q = segment_addr<L>(d, sp, sst, scol, g, row, col);
+    s.sha = uint32_t(q) & 15u;
+    s.a0 = load_vec((const RS_GLOBAL u32x4 *)(q & ~uint64_t(15)));
+    if (s.sha + (s.e1 - s.lo) > 16u) s.a1 = load_vec((const RS_GLOBAL u32x4 *)((q & ~uint64_t(15)) + 16u));
+    if (s.e1 < s.hi) {
+        if (send == rb) {  // the next row's first segment
+            ++row;
+            col = 0;
+            g = 0;
+        } else {
+            col = send;
+            ++g;
+        }
+        q = segment_addr<L>(d, sp, sst, scol, g, row, col);
+        s.shb = uint32_t(q) & 15u;
+        s.b0 = load_vec((const RS_GLOBAL u32x4 *)(q & ~uint64_t(15)));
+        if (s.shb + (s.hi - s.e1) > 16u) s.b1 = load_vec((const RS_GLOBAL u32x4 *)((q & ~uint64_t(15)) + 16u));
+    }
+}
+
+// v's bytes moved up by o (0..15): result byte j = v[j - o], zero below o.
+__device__ __forceinline__ u32x4 place_at(u32x4 v, uint32_t o) {
+    const u32x4 z = {0u, 0u, 0u, 0u};
+    return o == 0 ? v : funnel32(z, v, 16u - o);
+}
+
+__device__ __forceinline__ uint32_t pick_bytes(uint32_t a, uint32_t b, int32_t k) {
+    // bytes below k from a, from k on from b (k in 0..4)
+    if (k <= 0) return b;
+    if (k >= 4) return a;
+    const uint32_t m = (1u << (8 * k)) - 1u;
+    return (a & m) | (b & ~m);
+}
+
+__device__ __forceinline__ u32x4 uslot_compose(const USlot &s, uint32_t c0) {
+    u32x4 out = place_at(funnel32(s.a0, s.a1, s.sha), s.lo - c0);
+    if (s.e1 < s.hi) {
+        const u32x4 w = place_at(funnel32(s.b0, s.b1, s.shb), s.e1 - c0);
+        const int32_t o = int32_t(s.e1 - c0);
+        out.x = pick_bytes(out.x, w.x, o);
+        out.y = pick_bytes(out.y, w.y, o - 4);
+        out.z = pick_bytes(out.z, w.z, o - 8);
+        out.w = pick_bytes(out.w, w.w, o - 12);
+    }
+    return out;
+}
+
+__device__ __forceinline__ void uslot_store(RS_GLOBAL unsigned char *slot, u32x4 v, const USlot &s, uint32_t c0) {
+    if (s.lo == c0 && s.hi == c0 + 16u)
+        store_vec((RS_GLOBAL u32x4 *)slot, v);
+    else if (s.lo < s.hi)
+        store_partial(slot, v, s.lo - c0, s.hi - c0);
+}
+
+template <int L, int NPTR>
+__device__ __forceinline__ void run_gather_u(const Desc &d, const RS_CONST KArgs<NPTR> *a) {
+    const uint64_t *sp = reinterpret_cast<const uint64_t *>(rs_lds);
+    const uint32_t *sst = reinterpret_cast<const uint32_t *>(rs_lds + 8u * kMaxSegs);
+    const uint32_t *scol = reinterpret_cast<const uint32_t *>(rs_lds + 20u * kMaxSegs);
+    const RS_CONST int32_t *fan = (const RS_CONST int32_t *)(a->fan + d.fan_off);
+    const uint32_t nthr = blockDim.x, n = d.v1;
+    for (uint32_t ls = threadIdx.x; ls < n; ls += 2u * nthr) {
+        const uint32_t c0 = 16u * ls, c1 = c0 + 16u * nthr;
+        const bool has1 = ls + nthr < n;
+        USlot s0, s1;
+        uslot_load<L>(d, sp, sst, scol, c0, s0);
+        if (has1) uslot_load<L>(d, sp, sst, scol, c1, s1);
+        const u32x4 o0 = uslot_compose(s0, c0);
+        const u32x4 o1 = has1 ? uslot_compose(s1, c1) : o0;
+        for (uint32_t r = 0; r < d.nfan; ++r) {
+            RS_GLOBAL unsigned char *dst = (RS_GLOBAL unsigned char *)a->ptr[a->nsrc + uint32_t(fan[r])] + d.dst_base;
+            uslot_store(dst + c0, o0, s0, c0);
+            if (has1) uslot_store(dst + c1, o1, s1, c1);
+        }
+    }
+}
+
+template <int NPTR>
+__global__ __launch_bounds__(256) void reshard_gather_u_kernel(KArgs<NPTR> args) {
+    const RS_CONST KArgs<NPTR> *a = (const RS_CONST KArgs<NPTR> *)__builtin_amdgcn_kernarg_segment_ptr();
+    const uint32_t b = blockIdx.x;
+    const uint32_t idx = a->per_xcd ? (b & 7u) * a->per_xcd + (b >> 3) : b;
+    if (idx >= a->ndesc) return;
+    const Desc d = load_desc(a, idx);
+    stage_segments_u(d, a);
+    __syncthreads();
+    switch (kind_levels(d.kind)) {
+        case 1: run_gather_u<1>(d, a); break;
+        case 2: run_gather_u<2>(d, a); break;
+        default: run_gather_u<3>(d, a); break;
+    }
+}
+
 // Realignment chunks run in their own kernel so their register use does not
 // bound the direct kernel's occupancy.  STAGE: through LDS, else shifted loads.
 template <int NPTR, bool STAGE>
@@ -686,7 +848,8 @@ reshard_status_t launch(const Plan &p, const Desc *descs, const int32_t *fan, co
     const uint32_t cap_lds =
         p.tuning.cap_is_default ? residency_lds(p.direct_fanout <= 2 ? 16u : 12u, block) : user_lds;
     const uint32_t n_direct = uint32_t(p.n_direct), n_gather = uint32_t(p.n_gather);
-    const uint32_t n_realign = uint32_t(p.descs.size() - p.n_direct - p.n_gather);
+    const uint32_t n_gather_u = uint32_t(p.n_gather_u);
+    const uint32_t n_realign = uint32_t(p.descs.size() - p.n_direct - p.n_gather - p.n_gather_u);
     const uint32_t n_phase1 = uint32_t(p.n_phase1);
     if (n_phase1) {
         const reshard_status_t st = launch_one(reshard_kernel<NPTR>, a, n_phase1, remap, block, cap_lds, stream);
@@ -710,8 +873,20 @@ reshard_status_t launch(const Plan &p, const Desc *descs, const int32_t *fan, co
         const reshard_status_t st = launch_one(reshard_gather_kernel<NPTR>, a, n_gather, remap, block, glds, stream);
         if (st != RESHARD_OK) return st;
     }
-    if (n_realign) {
+    if (n_gather_u) {
+        uint32_t ulds = user_lds;
+        if (p.tuning.cap_is_default) {
+            const uint32_t fan = uint32_t(p.gather_u_fanout > 0 ? p.gather_u_fanout : 1);
+            ulds = residency_lds(64u / fan > 8u ? 64u / fan : 8u, block < 256u ? block : 256u);
+        }
         a.descs = descs + n_direct + n_gather;
+        const reshard_status_t st = launch_one(reshard_gather_u_kernel<NPTR>, a, n_gather_u, remap,
+                                               block < 256u ? block : 256u,
+                                               ulds > kGatherULds ? ulds : kGatherULds, stream);
+        if (st != RESHARD_OK) return st;
+    }
+    if (n_realign) {
+        a.descs = descs + n_direct + n_gather + n_gather_u;
         // Realignment kernels hide their load -> shift -> store latency with
         // resident workgroups: no residency cap (measured: capping at 12
         // waves per CU halves their throughput).  Staging takes its LDS.

@@ -596,6 +596,146 @@ bool lower_gather_group(Plan &p, const std::vector<size_t> &group, int64_t chunk
     return true;
 }
 
+// Unaligned row gather of one group (see desc.h): segments of any widths of
+// at least 16 bytes tiling the destination row, destination rows contiguous.
+// Returns false, emitting nothing, when the group does not qualify.
+bool lower_gather_unaligned(Plan &p, const std::vector<size_t> &group, int64_t chunk_bytes, std::vector<Desc> &out) {
+    const int nd = p.ndim;
+    const int64_t es = p.es;
+    if (nd < 1 || group.size() < 2 || group.size() > kMaxSegs) return false;
+    std::vector<size_t> g(group);
+    std::sort(g.begin(), g.end(), [&](size_t a, size_t b) { return p.tasks[a].lo[nd - 1] < p.tasks[b].lo[nd - 1]; });
+    const UnitTask &t0 = p.tasks[g[0]];
+    const int64_t fan_off = p.dst.shard_devs_off[t0.dst_shard];
+    const int64_t nfan = p.dst.shard_devs_off[t0.dst_shard + 1] - fan_off;
+    const int32_t rcv0 = p.dst.shard_devs[fan_off];
+    std::vector<int64_t> ext_d(nd), str_d(nd), dlo(nd);
+    for (int d = 0; d < nd; ++d) {
+        const int64_t jd = p.dst.dev_shard[int64_t(rcv0) * nd + d];
+        dlo[d] = p.dst.bounds[d][jd];
+        ext_d[d] = p.dst.bounds[d][jd + 1] - dlo[d];
+    }
+    for (int d = nd - 1; d >= 0; --d) str_d[d] = d == nd - 1 ? es : str_d[d + 1] * ext_d[d + 1];
+    // the segments tile the destination row, each at least 16 bytes
+    int64_t at = dlo[nd - 1];
+    for (size_t k : g) {
+        const UnitTask &t = p.tasks[k];
+        if (t.lo[nd - 1] != at || (t.hi[nd - 1] - t.lo[nd - 1]) * es < 16) return false;
+        at = t.hi[nd - 1];
+    }
+    if (at != dlo[nd - 1] + ext_d[nd - 1]) return false;
+    const int64_t row_bytes = ext_d[nd - 1] * es;
+    if (row_bytes >= (int64_t(1) << 31)) return false;
+    // destination rows contiguous: every outer extent but the outermost
+    // non-unit one spans its whole dimension
+    int64_t acc = row_bytes;
+    uint64_t rows = 1;
+    for (int d = nd - 2; d >= 0; --d) {
+        const int64_t n = t0.hi[d] - t0.lo[d];
+        if (n == 1) continue;
+        if (str_d[d] != acc) return false;
+        acc *= n;
+        rows *= uint64_t(n);
+    }
+    if (rows >= (uint64_t(1) << 31)) return false;
+    // source levels: drop unit extents, merge dims contiguous on every sender
+    const size_t ns = g.size();
+    std::vector<std::vector<int64_t>> str_s(ns, std::vector<int64_t>(nd)), slo(ns, std::vector<int64_t>(nd));
+    for (size_t k = 0; k < ns; ++k) {
+        const UnitTask &t = p.tasks[g[k]];
+        std::vector<int64_t> ext_s(nd);
+        for (int d = 0; d < nd; ++d) {
+            const int64_t js = p.src.dev_shard[int64_t(t.sender) * nd + d];
+            slo[k][d] = p.src.bounds[d][js];
+            ext_s[d] = p.src.bounds[d][js + 1] - slo[k][d];
+        }
+        for (int d = nd - 1; d >= 0; --d) str_s[k][d] = d == nd - 1 ? es : str_s[k][d + 1] * ext_s[d + 1];
+    }
+    struct SLevel {
+        int64_t n;
+        std::vector<int64_t> ss;
+    };
+    std::vector<SLevel> lv;  // innermost first
+    for (int d = nd - 2; d >= 0; --d) {
+        const int64_t n = t0.hi[d] - t0.lo[d];
+        if (n == 1) continue;
+        bool merge = !lv.empty();
+        for (size_t k = 0; k < ns && merge; ++k) merge = str_s[k][d] == lv.back().n * lv.back().ss[k];
+        if (merge) {
+            lv.back().n *= n;
+        } else {
+            SLevel l{n, std::vector<int64_t>(ns)};
+            for (size_t k = 0; k < ns; ++k) l.ss[k] = str_s[k][d];
+            lv.push_back(l);
+        }
+    }
+    if (lv.size() > 3) return false;
+    std::vector<Seg> seg(ns);
+    for (size_t k = 0; k < ns; ++k) {
+        const UnitTask &t = p.tasks[g[k]];
+        uint64_t so = 0, span = uint64_t((t.hi[nd - 1] - t.lo[nd - 1]) * es);
+        for (int d = 0; d < nd; ++d) so += uint64_t((t.lo[d] - slo[k][d]) * str_s[k][d]);
+        for (const auto &l : lv) span += uint64_t(l.n - 1) * uint64_t(l.ss[k]);
+        if (span >= (uint64_t(1) << 32)) return false;
+        seg[k] = Seg{so, {0u, 0u, 0u}, uint32_t(t.sender), uint32_t((t.lo[nd - 1] - dlo[nd - 1]) * es), 0u};
+        for (size_t i = 0; i < lv.size(); ++i) seg[k].ss[i] = uint32_t(uint64_t(lv[i].ss[k]));
+    }
+    uint64_t d0 = 0;  // the group's first byte in the receivers' buffers
+    for (int d = 0; d < nd - 1; ++d) d0 += uint64_t((t0.lo[d] - dlo[d]) * str_d[d]);
+    const uint64_t total = rows * uint64_t(row_bytes);
+    const int levels = std::max<int>(1, int(lv.size()));
+    Desc d{};
+    d.vpr = uint32_t(row_bytes);
+    d.n1 = lv.size() >= 2 ? uint32_t(lv[0].n) : 1u;
+    d.n2 = lv.size() >= 3 ? uint32_t(lv[1].n) : 1u;
+    const uint32_t wnom = uint32_t(row_bytes / int64_t(ns));
+    const FastDiv f0 = make_fastdiv(d.vpr), f1 = make_fastdiv(d.n1), f2 = make_fastdiv(d.n2), fw = make_fastdiv(wnom);
+    d.mul_vpr = f0.mul; d.sh_vpr = uint8_t(f0.shift);
+    d.mul_n1 = f1.mul;  d.sh_n1 = uint8_t(f1.shift);
+    d.mul_n2 = f2.mul;  d.sh_n2 = uint8_t(f2.shift);
+    d.run = wnom;
+    d.batch = fw.mul;
+    d.pad[2] = fw.shift;
+    d.kind = uint8_t(make_kind(4, uint32_t(levels)));
+    d.nfan = uint16_t(nfan);
+    d.fan_off = uint32_t(fan_off);
+    d.pad[0] = uint32_t(p.segs.size());
+    d.pad[1] = uint32_t(ns);
+    const uint64_t cv = uint64_t(std::max<int64_t>(16, chunk_bytes / 16)) / 16 * 16;
+    const uint64_t s_first = d0 / 16, s_end = (d0 + total + 15) / 16;
+    if (p.descs.size() + out.size() + (s_end - s_first + cv - 1) / cv > kMaxDescs) {
+        p.too_many = true;
+        return false;
+    }
+    std::vector<Desc> mine;
+    for (uint64_t s0 = s_first; s0 < s_end; s0 += cv) {
+        const uint64_t nsl = std::min(cv, s_end - s0), base = 16 * s0;
+        d.v0 = 0;
+        d.v1 = uint32_t(nsl);
+        d.dst_base = base;
+        uint32_t row0 = 0;
+        int64_t cofs0;
+        if (base <= d0) {
+            cofs0 = int64_t(base) - int64_t(d0);  // in (-16, 0]
+        } else {
+            const uint64_t q = base - d0;
+            row0 = uint32_t(q / uint64_t(row_bytes));
+            cofs0 = int64_t(q - uint64_t(row0) * uint64_t(row_bytes));
+        }
+        d.ss[0] = row0;
+        d.ss[1] = uint32_t(cofs0);
+        d.ss[2] = uint32_t(base < d0 ? d0 - base : 0);
+        d.src_rel0 = uint32_t(std::min<uint64_t>(16 * nsl, d0 + total - base));
+        mine.push_back(d);
+    }
+    p.segs.insert(p.segs.end(), seg.begin(), seg.end());
+    out.insert(out.end(), mine.begin(), mine.end());
+    p.align = std::max<int64_t>(p.align, 16);
+    p.max_fanout = std::max(p.max_fanout, nfan);
+    p.gather_u_fanout = std::max(p.gather_u_fanout, nfan);
+    return true;
+}
+
 void lower(Plan &p) {
     const int nd = p.ndim;
     const int64_t es = p.es;
@@ -613,7 +753,8 @@ void lower(Plan &p) {
     // dimension but the last (0x100: RESHARD_NO_GATHER; strategies copy per task).
     p.segs.clear();
     p.gather_fanout = 0;
-    std::vector<Desc> gdescs;
+    p.gather_u_fanout = 0;
+    std::vector<Desc> gdescs, udescs;
     std::vector<char> handled(p.tasks.size(), 0);
     if (!(p.flags & 0x100u) && !(p.flags & 0x60u)) {
         std::map<std::vector<int64_t>, std::vector<size_t>> groups;
@@ -627,7 +768,8 @@ void lower(Plan &p) {
             groups[key].push_back(i);
         }
         for (const auto &kv : groups)
-            if (lower_gather_group(p, kv.second, chunk, gdescs))
+            if (lower_gather_group(p, kv.second, chunk, gdescs) ||
+                lower_gather_unaligned(p, kv.second, chunk, udescs))
                 for (size_t i : kv.second) handled[i] = 1;
     }
 
@@ -729,6 +871,8 @@ void lower(Plan &p) {
     while (p.n_direct < p.descs.size() && !kind_realign(p.descs[p.n_direct].kind)) ++p.n_direct;
     p.descs.insert(p.descs.begin() + std::ptrdiff_t(p.n_direct), gdescs.begin(), gdescs.end());
     p.n_gather = gdescs.size();
+    p.descs.insert(p.descs.begin() + std::ptrdiff_t(p.n_direct + p.n_gather), udescs.begin(), udescs.end());
+    p.n_gather_u = udescs.size();
     p.n_phase1 = p.n_direct;
     if (p.flags & 0x20u) {
         // Send/recv analogue (Section 3.1): the sender's slice is read once

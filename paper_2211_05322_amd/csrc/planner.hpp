@@ -66,9 +66,11 @@ struct Plan {
     uint32_t lds_bytes = 0;    // LDS the realignment chunks need per workgroup
     size_t n_direct = 0;       // descs[0, n_direct): direct chunks
     size_t n_gather = 0;       // descs[n_direct, n_direct + n_gather): row-gather chunks;
+    size_t n_gather_u = 0;     // then n_gather_u unaligned row-gather chunks;
                                // the rest: realignment chunks
     std::vector<Seg> segs;     // row-gather segment entries
     int64_t gather_fanout = 0; // largest receiver count among row-gather chunks
+    int64_t gather_u_fanout = 0; // ... among unaligned row-gather chunks
     int64_t direct_fanout = 0; // largest receiver count among direct chunks
     size_t n_phase1 = 0;       // descs[0, n_phase1) run before descs[n_phase1, n_direct)
                                // (two launches; only the all-gather strategy has a second phase)

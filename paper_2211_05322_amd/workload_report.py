@@ -69,7 +69,8 @@ def report_row(key, w, steps, flush_steps, scratch, stream):
     plan_ms = (time.perf_counter() - t0) * 1e3
     st = B.reshard_plan_stats(plan)
     n_gather, n_realign = B.reshard_plan_gather_chunks(plan), B.reshard_plan_realign_chunks(plan)
-    n_direct = st["n_descriptors"] - n_gather - n_realign
+    n_gather_u = B.reshard_plan_unaligned_gather_chunks(plan)
+    n_direct = st["n_descriptors"] - n_gather - n_gather_u - n_realign
     dst = B.empty_shards(plan, 1)
     run = lambda: B.reshard_execute(plan, src, dst, stream=stream)  # noqa: E731
     for _ in range(5):
@@ -107,7 +108,7 @@ def report_row(key, w, steps, flush_steps, scratch, stream):
     ok = bool(torch.equal(back[0].view(torch.uint8), x.view(torch.uint8)))
     moved = st["bytes_read"] + st["bytes_written"]
     gbs = lambda us: moved / us / 1e3  # noqa: E731
-    kinds = "/".join(str(n) for n in (n_direct, n_gather, n_realign))
+    kinds = "/".join(str(n) for n in (n_direct, n_gather, n_gather_u, n_realign))
     row = (f"| {key} | {w.name} | {st['n_unit_tasks']} | {st['max_fanout']} | {kinds} | {moved / 1e6:.1f} | "
            f"{plan_ms:.2f} | {warm_us:.1f} | {100 * gbs(warm_us) / HBM_PEAK_GBS:.1f} | "
            f"{rot_us:.1f} ({nsets}) | {100 * gbs(rot_us) / HBM_PEAK_GBS:.1f} | "
@@ -134,7 +135,7 @@ def main():
     print(f"{torch.cuda.get_device_name(0)}; back-to-back: mean of {a.steps} launches; rotated: the same "
           f"over (n) buffer sets in turn; cold: mean of {a.flush_steps} launches, each after a read of "
           f"{a.flush_mib} MiB; % of {HBM_PEAK_GBS:.0f} GB/s\n")
-    print("| id | workload | unit tasks | fan-out | chunks direct/gather/realign | MB moved | plan ms | "
+    print("| id | workload | unit tasks | fan-out | chunks direct/gather/unaligned gather/realign | MB moved | plan ms | "
           "back-to-back µs | % | rotated µs (n) | % | cold µs | % | round trip |")
     print("|---" * 14 + "|")
     all_ok = True

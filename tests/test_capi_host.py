@@ -212,16 +212,18 @@ REALIGN_CASES = [
 @pytest.mark.parametrize("chunk", [0, 100, 5000])
 def test_host_realign_path(case, chunk):
     shape, dt, sm, ss, dm, ds = case
-    p = plan_of(shape, dt, sm, ss, dm, ds, chunk_bytes=chunk)
+    ng = B.RESHARD_NO_GATHER  # some cases take the unaligned row gather by default
+    p = plan_of(shape, dt, sm, ss, dm, ds, chunk_bytes=chunk, flags=ng)
     assert B.reshard_plan_realign_chunks(p) > 0, "case should take the realignment path"
     assert B.reshard_plan_lds_bytes(p) == 0
+    host_case(shape, dt, sm, ss, dm, ds, chunk_bytes=chunk, flags=ng)
     host_case(shape, dt, sm, ss, dm, ds, chunk_bytes=chunk)
-    q = plan_of(shape, dt, sm, ss, dm, ds, flags=B.RESHARD_NO_REALIGN)
+    q = plan_of(shape, dt, sm, ss, dm, ds, flags=B.RESHARD_NO_REALIGN | ng)
     assert B.reshard_plan_realign_chunks(q) == 0
-    host_case(shape, dt, sm, ss, dm, ds, flags=B.RESHARD_NO_REALIGN)
-    r = plan_of(shape, dt, sm, ss, dm, ds, flags=B.RESHARD_LDS_STAGING)
+    host_case(shape, dt, sm, ss, dm, ds, flags=B.RESHARD_NO_REALIGN | ng)
+    r = plan_of(shape, dt, sm, ss, dm, ds, flags=B.RESHARD_LDS_STAGING | ng)
     assert B.reshard_plan_lds_bytes(r) > 0
-    host_case(shape, dt, sm, ss, dm, ds, flags=B.RESHARD_LDS_STAGING, chunk_bytes=chunk)
+    host_case(shape, dt, sm, ss, dm, ds, flags=B.RESHARD_LDS_STAGING | ng, chunk_bytes=chunk)
 
 
 def test_aligned_workloads_do_not_realign():
@@ -365,6 +367,42 @@ def test_gather_band_chunk_count():
         per_row = [min(b, nseg - b0) * row_slots // nseg for b0 in range(0, nseg, b)]
         want = 8 * sum(-(-rows * w // (cb // 16)) for w in per_row)
         assert B.reshard_plan_gather_chunks(p) == want, band
+
+
+# ------------------------------------------------ unaligned row gather
+
+UNALIGNED_GATHER_CASES = [
+    # segments of any width >= 16 bytes, any 16-byte phase, contiguous destination rows
+    ((2, 64, 12300), "float16", (4, 8), "RRS^{01}", (4, 8), "RS^1R"),  # 770/768-byte segments, 24600-byte rows
+    ((6, 4000), "float16", (3,), "RS^0", (2,), "RS^0"),                 # uneven cut of 2000 by 1334
+    ((4, 32, 1000), "float16", (1, 4), "RRS^1", (2,), "RRR"),           # 500-byte segments, fan-out 2
+    ((3, 10, 7, 333), "float32", (2, 3), "RRRS^{01}", (3,), "S^0RRR"),  # 6 senders of 222/220 bytes
+    ((5, 1000), "uint8", (4,), "RS^0", (1,), "RR"),                     # byte elements, 250-byte segments
+    ((2, 5, 8, 12), "float64", (2, 2), "RRRS^{01}", (2,), "RRRR"),      # 24-byte segments
+]
+
+
+@pytest.mark.parametrize("case", UNALIGNED_GATHER_CASES)
+@pytest.mark.parametrize("chunk", [0, 64, 3000])
+def test_host_unaligned_gather(case, chunk):
+    shape, dt, sm, ss, dm, ds = case
+    p = plan_of(shape, dt, sm, ss, dm, ds, chunk_bytes=chunk)
+    assert B.reshard_plan_unaligned_gather_chunks(p) > 0, "case should take the unaligned row gather"
+    assert B.reshard_plan_gather_chunks(p) == 0
+    host_case(shape, dt, sm, ss, dm, ds, chunk_bytes=chunk)
+    q = plan_of(shape, dt, sm, ss, dm, ds, flags=B.RESHARD_NO_GATHER)
+    assert B.reshard_plan_unaligned_gather_chunks(q) == 0
+    host_case(shape, dt, sm, ss, dm, ds, flags=B.RESHARD_NO_GATHER)
+
+
+def test_unaligned_gather_declines():
+    # segments under 16 bytes, or destination rows that are not contiguous:
+    # per-task chunks instead
+    for case in (((4, 8, 40), "float16", (8,), "RRS^0", (2,), "S^0RR"),
+                 ((6, 10, 300), "float16", (2, 3), "RS^0S^1", (2,), "RRS^0")):
+        p = plan_of(*case)
+        assert B.reshard_plan_unaligned_gather_chunks(p) == 0
+        host_case(*case)
 
 
 def test_gather_used_by_column_split_workloads():

@@ -246,25 +246,28 @@ from tests.test_capi_host import REALIGN_CASES  # noqa: E402
 def test_realign_path(case):
     shape, dt, sm, ss, dm, ds = case
     _say(f"realign {case}")
-    assert B.reshard_plan_realign_chunks(B.reshard_plan(shape, dt, sm, ss, dm, ds)) > 0
-    for kw in ({}, {"chunk_bytes": 100, "block_threads": 64}, {"chunk_bytes": 5000, "block_threads": 1024},
-               {"max_wgs_per_cu": -1}, {"flags": B.RESHARD_TASK_ORDER | B.RESHARD_XCD_REMAP},
-               {"flags": B.RESHARD_NO_REALIGN}, {"flags": B.RESHARD_LDS_STAGING},
-               {"flags": B.RESHARD_LDS_STAGING, "chunk_bytes": 300, "block_threads": 64}):
+    ng = B.RESHARD_NO_GATHER  # some cases take the unaligned row gather by default
+    assert B.reshard_plan_realign_chunks(B.reshard_plan(shape, dt, sm, ss, dm, ds, flags=ng)) > 0
+    for kw in ({}, {"flags": ng}, {"chunk_bytes": 100, "block_threads": 64, "flags": ng},
+               {"chunk_bytes": 5000, "block_threads": 1024, "flags": ng},
+               {"max_wgs_per_cu": -1, "flags": ng}, {"flags": B.RESHARD_TASK_ORDER | B.RESHARD_XCD_REMAP | ng},
+               {"flags": B.RESHARD_NO_REALIGN | ng}, {"flags": B.RESHARD_LDS_STAGING | ng},
+               {"flags": B.RESHARD_LDS_STAGING | ng, "chunk_bytes": 300, "block_threads": 64}):
         got, want = run_gpu(shape, dt, sm, ss, dm, ds, rand_bits(shape, dt, 5), **kw)
         assert_same(got, want)
 
 
 def test_realign_uneven_large():
     # fp16 [4, 512, 12300] over 32 shards of the last dim (385 or 384 wide):
-    # every row phase differs between the two layouts; mixed direct and
-    # realignment chunks in one execute
+    # every row phase differs between the two layouts; by default the
+    # unaligned row gather, else mixed direct and realignment chunks
     shape = (4, 512, 12300)
     sm, ss, dm, ds = (4, 8), "RRS^{01}", (4, 8), "RS^1R"
     _say("realign uneven large")
-    p = B.reshard_plan(shape, "float16", sm, ss, dm, ds)
+    p = B.reshard_plan(shape, "float16", sm, ss, dm, ds, flags=B.RESHARD_NO_GATHER)
     assert B.reshard_plan_realign_chunks(p) > 0
-    for flags in (0, B.RESHARD_LDS_STAGING):
+    assert B.reshard_plan_unaligned_gather_chunks(B.reshard_plan(shape, "float16", sm, ss, dm, ds)) > 0
+    for flags in (0, B.RESHARD_NO_GATHER, B.RESHARD_NO_GATHER | B.RESHARD_LDS_STAGING):
         got, want = run_gpu(shape, "float16", sm, ss, dm, ds, rand_bits(shape, "float16", 6), flags=flags)
         assert_same(got, want)
 
@@ -314,6 +317,23 @@ def test_gather_path(case):
         assert_same(got, want)
 
 
+# ------------------------------------------------- unaligned row gather
+
+from tests.test_capi_host import UNALIGNED_GATHER_CASES  # noqa: E402
+
+
+@pytest.mark.parametrize("case", UNALIGNED_GATHER_CASES)
+def test_unaligned_gather_path(case):
+    shape, dt, sm, ss, dm, ds = case
+    _say(f"unaligned gather {case}")
+    assert B.reshard_plan_unaligned_gather_chunks(B.reshard_plan(shape, dt, sm, ss, dm, ds)) > 0
+    for kw in ({}, {"chunk_bytes": 64, "block_threads": 64}, {"chunk_bytes": 3000, "block_threads": 1024},
+               {"max_wgs_per_cu": -1}, {"max_wgs_per_cu": 2}, {"flags": B.RESHARD_XCD_REMAP},
+               {"flags": B.RESHARD_NO_GATHER}):
+        got, want = run_gpu(shape, dt, sm, ss, dm, ds, rand_bits(shape, dt, 14), **kw)
+        assert_same(got, want)
+
+
 # ------------------------------------------------------------ maximum sizes
 
 def test_max_buffers_direct_and_gather():
@@ -349,6 +369,8 @@ def _check_against_boxes(x, dst, shape, mesh, spec):
     ((5, 1 << 29), (2,), "RS^0", (1,), "RR"),
     # rows of 2^30 + 10 bytes split unevenly: different 16-byte phases, 5 GiB source
     ((5, (1 << 29) + 5), (1,), "RR", (2,), "RS^0"),
+    # the same rows gathered from two uneven, misaligned column halves into one 5 GiB buffer
+    ((5, (1 << 29) + 5), (2,), "RS^0", (1,), "RR"),
 ])
 def test_over_4gib(case):
     """Buffers above 4 GiB: every destination compared, element by element on
