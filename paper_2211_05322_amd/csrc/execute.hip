@@ -683,13 +683,16 @@ __device__ __forceinline__ void uslot_store(RS_GLOBAL unsigned char *slot, u32x4
         store_partial(slot, v, s.lo - c0, s.hi - c0);
 }
 
-template <int L, int NPTR>
+// RF > 0: compile-time receiver count (vector-major stores up to 4
+// receivers, as the aligned gather); RF == 0: runtime count.
+template <int L, int RF, int NPTR>
 __device__ __forceinline__ void run_gather_u(const Desc &d, const RS_CONST KArgs<NPTR> *a) {
     const uint64_t *sp = reinterpret_cast<const uint64_t *>(rs_lds);
     const uint32_t *sst = reinterpret_cast<const uint32_t *>(rs_lds + 8u * kMaxSegs);
     const uint32_t *scol = reinterpret_cast<const uint32_t *>(rs_lds + 20u * kMaxSegs);
     const RS_CONST int32_t *fan = (const RS_CONST int32_t *)(a->fan + d.fan_off);
     const uint32_t nthr = blockDim.x, n = d.v1;
+    const uint32_t nr = RF > 0 ? uint32_t(RF) : d.nfan;
     for (uint32_t ls = threadIdx.x; ls < n; ls += 2u * nthr) {
         const uint32_t c0 = 16u * ls, c1 = c0 + 16u * nthr;
         const bool has1 = ls + nthr < n;
@@ -698,11 +701,40 @@ __device__ __forceinline__ void run_gather_u(const Desc &d, const RS_CONST KArgs
         if (has1) uslot_load<L>(d, sp, sst, scol, c1, s1);
         const u32x4 o0 = uslot_compose(s0, c0);
         const u32x4 o1 = has1 ? uslot_compose(s1, c1) : o0;
-        for (uint32_t r = 0; r < d.nfan; ++r) {
-            RS_GLOBAL unsigned char *dst = (RS_GLOBAL unsigned char *)a->ptr[a->nsrc + uint32_t(fan[r])] + d.dst_base;
-            uslot_store(dst + c0, o0, s0, c0);
-            if (has1) uslot_store(dst + c1, o1, s1, c1);
+        if (RF >= 1 && RF <= 4) {
+#pragma unroll
+            for (uint32_t r = 0; r < nr; ++r)
+                uslot_store((RS_GLOBAL unsigned char *)a->ptr[a->nsrc + uint32_t(fan[r])] + d.dst_base + c0, o0, s0, c0);
+            if (has1) {
+#pragma unroll
+                for (uint32_t r = 0; r < nr; ++r)
+                    uslot_store((RS_GLOBAL unsigned char *)a->ptr[a->nsrc + uint32_t(fan[r])] + d.dst_base + c1, o1, s1,
+                                c1);
+            }
+        } else {
+#pragma unroll
+            for (uint32_t r = 0; r < nr; ++r) {
+                RS_GLOBAL unsigned char *dst =
+                    (RS_GLOBAL unsigned char *)a->ptr[a->nsrc + uint32_t(fan[r])] + d.dst_base;
+                uslot_store(dst + c0, o0, s0, c0);
+                if (has1) uslot_store(dst + c1, o1, s1, c1);
+            }
         }
+    }
+}
+
+template <int L, int NPTR>
+__device__ __forceinline__ void run_gather_u_fan(const Desc &d, const RS_CONST KArgs<NPTR> *a) {
+    switch (d.nfan) {
+        case 1: run_gather_u<L, 1>(d, a); break;
+        case 2: run_gather_u<L, 2>(d, a); break;
+        case 3: run_gather_u<L, 3>(d, a); break;
+        case 4: run_gather_u<L, 4>(d, a); break;
+        case 5: run_gather_u<L, 5>(d, a); break;
+        case 6: run_gather_u<L, 6>(d, a); break;
+        case 7: run_gather_u<L, 7>(d, a); break;
+        case 8: run_gather_u<L, 8>(d, a); break;
+        default: run_gather_u<L, 0>(d, a); break;
     }
 }
 
@@ -716,9 +748,9 @@ __global__ __launch_bounds__(256) void reshard_gather_u_kernel(KArgs<NPTR> args)
     stage_segments_u(d, a);
     __syncthreads();
     switch (kind_levels(d.kind)) {
-        case 1: run_gather_u<1>(d, a); break;
-        case 2: run_gather_u<2>(d, a); break;
-        default: run_gather_u<3>(d, a); break;
+        case 1: run_gather_u_fan<1>(d, a); break;
+        case 2: run_gather_u_fan<2>(d, a); break;
+        default: run_gather_u_fan<3>(d, a); break;
     }
 }
 
