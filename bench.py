@@ -92,7 +92,8 @@ def main():
     ap.add_argument("--steps", type=int, default=50)
     ap.add_argument("--warmup", type=int, default=5)
     ap.add_argument("--config", default=None,
-                    help="workload id 1..5 (default 5), or fanoutR (1 GiB, one sender to R replicas)")
+                    help="workload id 1..5 (default 5), uneven5 / uneven3 (workloads 5 / 3 with an uneven last "
+                         "dimension), or fanoutR (1 GiB, one sender to R replicas)")
     ap.add_argument("--strategy", choices=["broadcast", "sendrecv", "allgather"], default="broadcast",
                     help="broadcast (default) or a comparison strategy that re-reads slices per receiver")
     ap.add_argument("--seed", type=int, default=0)

@@ -2,8 +2,9 @@
 
     python -m paper_2211_05322_amd.workload_report [--steps 50] [--flush-steps 20] [--flush-mib 1024]
 
-For each workload (the five resharding tasks, then the one-sender
-replication microbenchmark at 1, 4 and 8 receivers) prints one markdown row:
+For each workload (the five resharding tasks, workloads 5 and 3 with an
+uneven last dimension, then the one-sender replication microbenchmark at 1,
+4 and 8 receivers) prints one markdown row:
 unit tasks, fan-out, chunks per kernel, bytes moved (read + write), planning
 time, and three timings of `reshard_execute`:
 
@@ -30,7 +31,7 @@ import time
 import torch
 
 from . import binding as B
-from .workloads import WORKLOADS, fanout_workload, make_workload_tensor
+from .workloads import make_workload_tensor, workload_by_name
 
 HBM_PEAK_GBS = 8000.0
 
@@ -124,7 +125,7 @@ def main():
     ap.add_argument("--steps", type=int, default=50)
     ap.add_argument("--flush-steps", type=int, default=20)
     ap.add_argument("--flush-mib", type=int, default=1024)
-    ap.add_argument("--workloads", default="1,2,3,4,5,fanout1,fanout4,fanout8")
+    ap.add_argument("--workloads", default="1,2,3,4,5,uneven5,uneven3,fanout1,fanout4,fanout8")
     a = ap.parse_args()
     if not torch.cuda.is_available():
         raise SystemExit("no GPU visible")
@@ -140,7 +141,7 @@ def main():
     print("|---" * 14 + "|")
     all_ok = True
     for key in a.workloads.split(","):
-        w = fanout_workload(int(key[len("fanout"):])) if key.startswith("fanout") else WORKLOADS[int(key)]
+        w = workload_by_name(key)
         row, ok = report_row(key, w, a.steps, a.flush_steps, scratch, stream)
         all_ok &= ok
         print(row, flush=True)

@@ -61,6 +61,16 @@ WORKLOADS = {
 # The resharding the benchmark times: the largest tensor (403 MB, 2.01 GB moved).
 BENCH_WORKLOAD = 5
 
+# Workloads 5 and 3 with a last dimension that the shard count does not
+# divide: the balanced split gives segments of two widths whose rows sit in
+# different 16-byte phases on the two sides (the unaligned row-gather path).
+UNEVEN_WORKLOADS = {
+    "uneven5": Workload("gpt3_act_fp16_8x2048x12300_hidden32_uneven_to_seq8x4rep", (8, 2048, 12300), "float16",
+                        "normal", (4, 8), "R R S^{01}", (4, 8), "R S^1 R"),
+    "uneven3": Workload("fp16_16x2048x5130_s01_uneven_to_replicated", (16, 2048, 5130), "float16", "normal",
+                        (2, 4), "R R S^{01}", (2, 4), "R R R"),
+}
+
 
 # The multi-to-multi microbenchmark of the paper's Table 3: tensor
 # (1024, 1024, 512), (case, send spec, recv spec, send mesh, recv mesh); a
@@ -91,10 +101,12 @@ def fanout_workload(receivers, nbytes=1 << 30):
 
 
 def workload_by_name(key):
-    """WORKLOADS id (1..5 or "1".."5") or "fanoutR" (R receivers, 1 GiB)."""
+    """WORKLOADS id (1..5 or "1".."5"), an UNEVEN_WORKLOADS key, or "fanoutR" (R receivers, 1 GiB)."""
     key = str(key)
     if key.startswith("fanout"):
         return fanout_workload(int(key[len("fanout"):]))
+    if key in UNEVEN_WORKLOADS:
+        return UNEVEN_WORKLOADS[key]
     return WORKLOADS[int(key)]
 
 

@@ -15,7 +15,8 @@ import torch
 
 import oracle
 from paper_2211_05322_amd import binding as B
-from paper_2211_05322_amd.workloads import WORKLOADS, as_numpy_bits, make_workload_tensor
+from paper_2211_05322_amd.workloads import (UNEVEN_WORKLOADS, WORKLOADS, as_numpy_bits, make_workload_tensor,
+                                            workload_by_name)
 from tests.test_capi_host import _fuzz
 from tests.test_oracle_pins import fmt_spec, random_dims
 
@@ -211,10 +212,10 @@ def test_plan_reuse_on_streams():
             assert np.array_equal(d.cpu().numpy().view(np.uint32), w)
 
 
-@pytest.mark.parametrize("wid", sorted(WORKLOADS))
+@pytest.mark.parametrize("wid", sorted(WORKLOADS) + sorted(UNEVEN_WORKLOADS))
 def test_workload_full_size(wid):
     """Full-size workload, bench launch configuration, every output compared."""
-    w = WORKLOADS[wid]
+    w = workload_by_name(wid)
     _say(f"workload {wid} {w.name} {w.shape}")
     x = make_workload_tensor(w, seed=0)
     xb = as_numpy_bits(x)
