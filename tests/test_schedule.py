@@ -55,6 +55,25 @@ def test_oracle_against_exhaustive_search(seed):
         assert sched["makespan"] == max(s + m[0] for s, m in zip(sched["start"], model))
 
 
+@pytest.mark.parametrize("seed", range(6))
+def test_dfs_reaches_exhaustive_optimum_on_eight_tasks(seed):
+    # 8 tasks with their sender host fixed: the optimum is the best of the
+    # 8! orders; 6 tasks with two candidate senders each: 6! x 2^6 schedules
+    rng = random.Random(100 + seed)
+    for n, ncand in ((8, 1), (6, 2)):
+        model = []
+        for _ in range(n):
+            cand = sorted(rng.sample(range(3), ncand))
+            recv = sorted(rng.sample(range(3, 6), rng.randint(1, 2)))
+            model.append((rng.choice([1, 2, 3, 5]), cand, recv))
+        opt = S.optimum(model, 6)
+        full = S.dfs(model, 6, 10**9)
+        assert full["makespan"] == opt and S.valid(model, full)
+        assert S.lower_bound(model, 6) <= opt
+        for sched in (S.naive(model, 6), S.load_balance(model, 6), S.randomized(model, 6, 8, seed)):
+            assert S.valid(model, sched) and sched["makespan"] >= opt
+
+
 def test_lower_bound_is_tight_when_one_host_carries_everything():
     model = [(3, [0], [2]), (4, [1], [2]), (5, [0, 1], [2])]
     assert S.lower_bound(model, 3) == 12 == S.optimum(model, 3)
