@@ -149,7 +149,8 @@ def main():
     st = B.reshard_plan_stats(plan)
     dst = B.empty_shards(plan, 1)
     footprint = sum(t.numel() * t.element_size() for t in src + dst)
-    nsets = args.buffer_sets or min(64, max(2, -(-(4 << 30) // max(footprint, 1))))
+    nsets = args.buffer_sets or min(64, args.steps, max(2, -(-(4 << 30) // max(footprint, 1))))
+    nsets = max(1, nsets)
     sets = [(src, dst)]
     for _ in range(nsets - 1):
         s2 = B.empty_shards(scatter, 1)
@@ -173,12 +174,12 @@ def main():
     ms_total = ev0.elapsed_time(ev1)
     ms_per_step = ms_total / args.steps
 
-    # Round-trip check through the library: every set's dst -> one buffer
-    # must equal x.
+    # Round-trip check through the library: the dst of every set a step
+    # wrote -> one buffer must equal x.
     back_plan = B.reshard_plan(w.shape, w.dtype, w.dst_mesh, w.dst_spec, (1,), rep, block_threads=1024)
     back = B.empty_shards(back_plan, 1)
     roundtrip_ok = True
-    for _, d_ in sets:
+    for _, d_ in sets[:min(nsets, max(args.warmup, args.steps))]:
         B.reshard_execute(back_plan, d_, back)
         torch.cuda.synchronize()
         roundtrip_ok &= bool(torch.equal(back[0].view(torch.uint8), x.view(torch.uint8)))
