@@ -155,16 +155,29 @@ reshard_status_t reshard_plan_ex(int ndim, const int64_t *shape, reshard_dtype_t
  * reshard_plan_alignment() bytes.  Source and destination buffers must not
  * overlap.  `stream` is a hipStream_t (NULL = the null stream).
  *
- * Asynchronous and stream-ordered: it enqueues one kernel and returns.  The
- * first call on a device uploads the descriptor table to memory the plan owns
- * (one hipMalloc + synchronous copy); later calls only launch.  A plan may be
- * executed any number of times, on any stream; calls on different streams
- * that write the same destination buffers race, as any two kernels would.
+ * Asynchronous and stream-ordered: it enqueues one kernel per kind of chunk
+ * the plan holds (one for every workload of the paper's shapes) and returns.
+ * The first call on a device uploads the descriptor table to memory the plan
+ * owns (one hipMalloc + synchronous copies) unless reshard_plan_upload did;
+ * later calls only launch, so they can be captured into a HIP graph.  A plan
+ * may be executed any number of times, on any stream; calls on different
+ * streams that write the same destination buffers race, as any two kernels
+ * would.
  *
  * Errors: EINVAL for NULL plan or pointer arrays, a NULL or misaligned buffer
  * for a non-empty shard; ENOMEM if the table upload cannot allocate; EHIP if a
  * HIP call or the launch fails.
  */
+/*
+ * Upload the plan's descriptor, receiver and segment tables to the current
+ * HIP device (one hipMalloc + synchronous copies; nothing if already done
+ * on that device).  After it, reshard_execute on that device allocates and
+ * copies nothing, so it can run under HIP graph capture.  Errors: EINVAL
+ * for a NULL plan, ENOMEM if the allocation fails, EHIP if a HIP call
+ * fails.
+ */
+reshard_status_t reshard_plan_upload(const reshard_plan_t *plan);
+
 reshard_status_t reshard_execute(const reshard_plan_t *plan, void *const *src_ptrs,
                                  void *const *dst_ptrs, void *stream);
 

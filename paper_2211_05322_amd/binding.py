@@ -78,6 +78,8 @@ def load(path=None):
     lib.reshard_plan_alignment.restype = ctypes.c_int64
     lib.reshard_plan_lds_bytes.argtypes = [ctypes.c_void_p]
     lib.reshard_plan_lds_bytes.restype = ctypes.c_int64
+    lib.reshard_plan_upload.argtypes = [ctypes.c_void_p]
+    lib.reshard_plan_upload.restype = ctypes.c_int
     lib.reshard_plan_gather_chunks.argtypes = [ctypes.c_void_p]
     lib.reshard_plan_gather_chunks.restype = ctypes.c_int64
     lib.reshard_plan_realign_chunks.argtypes = [ctypes.c_void_p]
@@ -186,6 +188,11 @@ def _stream_handle(stream):
     if isinstance(stream, int):
         return stream
     return stream.cuda_stream
+
+
+def reshard_plan_upload(plan):
+    """Upload the plan's tables to the current device (then execute is graph-capturable)."""
+    _check(load().reshard_plan_upload(plan.handle))
 
 
 def reshard_execute(plan, src_bufs, dst_bufs, stream=None):

@@ -950,6 +950,20 @@ void release_device_table(const Plan &p) {
 
 }  // namespace rs
 
+extern "C" reshard_status_t reshard_plan_upload(const reshard_plan_t *plan) {
+    using namespace rs;
+    const Plan *p = reinterpret_cast<const Plan *>(plan);
+    if (!p) return fail(RESHARD_EINVAL, "NULL plan");
+    if (p->descs.empty()) return RESHARD_OK;
+    int dev = -1;
+    const hipError_t e = hipGetDevice(&dev);
+    if (e != hipSuccess) return fail(RESHARD_EHIP, std::string("hipGetDevice: ") + hipGetErrorString(e));
+    const Desc *descs = nullptr;
+    const int32_t *fan = nullptr;
+    const Seg *segs = nullptr;
+    return device_table(*p, dev, &descs, &fan, &segs);
+}
+
 extern "C" reshard_status_t reshard_execute(const reshard_plan_t *plan, void *const *src_ptrs,
                                             void *const *dst_ptrs, void *stream) {
     using namespace rs;

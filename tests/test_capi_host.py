@@ -269,6 +269,10 @@ def test_plan_error_ndim_and_nulls():
     assert "1..8" in B.reshard_last_error()
     lib.reshard_plan_destroy(None)  # NULL accepted
     assert lib.reshard_execute(None, None, None, None) == B.RESHARD_EINVAL
+    assert lib.reshard_plan_upload(None) == B.RESHARD_EINVAL
+    # a plan with nothing to move has no table: uploading it touches no device
+    empty = plan_of((0, 4), "float16", (2,), "S^0R", (2,), "RS^0")
+    assert lib.reshard_plan_upload(empty.handle) == B.RESHARD_OK
 
 
 def test_query_errors():
@@ -283,6 +287,8 @@ def test_query_errors():
     for cap in (1, 33, -2):
         with pytest.raises(B.ReshardError):
             B.reshard_plan((4, 4), "float16", (2,), "RR", (2,), "RR", max_wgs_per_cu=cap)
+    with pytest.raises(B.ReshardError):
+        B.reshard_plan((4, 4), "float16", (2,), "RR", (2,), "RR", gather_band=-1)
 
 
 def test_execute_rejects_null_buffer_on_host_interpreter():
