@@ -344,6 +344,7 @@ GATHER_CASES = [
     ((6, 8, 10, 256), "float16", (2, 2), "RRRS^{01}", (3,), "RS^0RR"),
     ((16, 4, 96), "float64", (3,), "RRS^0", (2, 2), "S^0RR"),
     ((2, 64, 1024), "float16", (4, 8), "RRS^{01}", (4, 8), "RS^1R"),
+    ((2, 8, 640), "float16", (1, 4), "RRS^1", (3, 4), "RRR"),                # fan-out 12: runtime receiver loop
 ]
 
 
@@ -385,6 +386,8 @@ UNALIGNED_GATHER_CASES = [
     ((3, 10, 7, 333), "float32", (2, 3), "RRRS^{01}", (3,), "S^0RRR"),  # 6 senders of 222/220 bytes
     ((5, 1000), "uint8", (4,), "RS^0", (1,), "RR"),                     # byte elements, 250-byte segments
     ((2, 5, 8, 12), "float64", (2, 2), "RRRS^{01}", (2,), "RRRR"),      # 24-byte segments
+    ((2, 8, 650), "float16", (1, 4), "RRS^1", (3, 4), "RRR"),           # fan-out 12: runtime receiver loop
+    ((3, 16, 1000), "uint8", (5,), "RRS^0", (2, 5), "RRR"),             # fan-out 10, 200-byte segments
 ]
 
 
