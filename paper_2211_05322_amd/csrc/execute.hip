@@ -1,13 +1,24 @@
-// execute.hip -- the fused pack / multicast / unpack kernel for gfx950 and
-// reshard_execute.
+// execute.hip -- the resharding kernels for gfx950 and reshard_execute.
 //
-// One workgroup runs one descriptor (a chunk of one piece of one unit task).
-// Each lane moves W-byte vectors: one load from the sender's buffer, then the
-// same vector is stored to every receiver at the same local offset -- the
-// broadcast strategy of Section 3.1 (one sender per slice, every receiver
-// gets it) with the source read exactly once.  Loads of a batch of U vectors
-// are issued before any of their stores so each lane keeps U loads in flight.
-// No arithmetic is done on the data, so no MFMA: the kernel is bound by HBM.
+// Every kernel moves bytes from senders' buffers to receivers' buffers in the
+// broadcast strategy of Section 3.1: each unique slice is read once and every
+// receiver gets the same bytes at the same local offset.  One workgroup runs
+// one descriptor (a chunk); an execute launches one kernel per kind of chunk
+// the plan holds:
+//   reshard_kernel          direct chunks: a range of W-byte vectors of one
+//                           piece of one unit task (source and destination in
+//                           the same 16-byte phase);
+//   reshard_gather_kernel   row gather: 16-byte slots of whole destination
+//                           rows, each from the sender owning its column
+//                           segment (equal, 16-byte aligned segments);
+//   reshard_gather_u_kernel unaligned row gather: 16-byte slots of the
+//                           receivers' buffers built from at most two
+//                           misaligned pieces (segments of any width >= 16 B);
+//   reshard_realign_kernel  rows in different 16-byte phases, one task at a
+//                           time (shifted loads, or staging through LDS).
+// Loads of a batch are issued before its stores so each lane keeps several
+// loads in flight.  No arithmetic is done on the data, so no MFMA: the
+// kernels are bound by HBM.
 //
 // Pointer tables travel in the kernel arguments (no per-call upload); the
 // descriptor table and receiver lists are read through the constant address
@@ -81,6 +92,19 @@ __device__ __forceinline__ void store_vec(RS_GLOBAL V *p, V x) {
 #ifndef RS_STORE_ORDER
 #define RS_STORE_ORDER 0  // 0: receiver-major stores, 1: vector-major stores
 #endif
+
+// Descriptor idx, loaded with a uniform index through the constant address
+// space so it lands in scalar registers.
+template <int NPTR>
+__device__ __forceinline__ Desc load_desc(const RS_CONST KArgs<NPTR> *a, uint32_t idx) {
+    const RS_CONST u32x4 *q = (const RS_CONST u32x4 *)(a->descs + idx);
+    u32x4 raw[sizeof(Desc) / 16];
+#pragma unroll
+    for (int i = 0; i < int(sizeof(Desc) / 16); ++i) raw[i] = q[i];
+    Desc d;
+    __builtin_memcpy(&d, raw, sizeof(Desc));
+    return d;
+}
 
 // Load one batch of U vectors per lane (vectors v, v+nthr, ...).  FULL: the
 // whole batch is inside the chunk (a workgroup-uniform fact), so no lane
@@ -321,13 +345,7 @@ __global__ __launch_bounds__(1024) void reshard_kernel(KArgs<NPTR> args) {
     const uint32_t b = blockIdx.x;
     const uint32_t idx = a->per_xcd ? (b & 7u) * a->per_xcd + (b >> 3) : b;
     if (idx >= a->ndesc) return;
-    // uniform load through the constant address space -> scalar registers
-    const RS_CONST u32x4 *q = (const RS_CONST u32x4 *)(a->descs + idx);
-    u32x4 raw[sizeof(Desc) / 16];
-#pragma unroll
-    for (int i = 0; i < int(sizeof(Desc) / 16); ++i) raw[i] = q[i];
-    Desc d;
-    __builtin_memcpy(&d, raw, sizeof(Desc));
+    const Desc d = load_desc(a, idx);
     switch (d.kind) {
         case make_kind(4, 1): run_wide<1>(d, a); break;
         case make_kind(4, 2): run_wide<2>(d, a); break;
@@ -526,17 +544,6 @@ __device__ __forceinline__ void run_gather_fan(const Desc &d, const RS_CONST KAr
         case 8: run_gather<L, 8>(d, a); break;
         default: run_gather<L, 0>(d, a); break;
     }
-}
-
-template <int NPTR>
-__device__ __forceinline__ Desc load_desc(const RS_CONST KArgs<NPTR> *a, uint32_t idx) {
-    const RS_CONST u32x4 *q = (const RS_CONST u32x4 *)(a->descs + idx);
-    u32x4 raw[sizeof(Desc) / 16];
-#pragma unroll
-    for (int i = 0; i < int(sizeof(Desc) / 16); ++i) raw[i] = q[i];
-    Desc d;
-    __builtin_memcpy(&d, raw, sizeof(Desc));
-    return d;
 }
 
 template <int NPTR>
@@ -762,12 +769,7 @@ __global__ __launch_bounds__(256) void reshard_realign_kernel(KArgs<NPTR> args) 
     const uint32_t b = blockIdx.x;
     const uint32_t idx = a->per_xcd ? (b & 7u) * a->per_xcd + (b >> 3) : b;
     if (idx >= a->ndesc) return;
-    const RS_CONST u32x4 *q = (const RS_CONST u32x4 *)(a->descs + idx);
-    u32x4 raw[sizeof(Desc) / 16];
-#pragma unroll
-    for (int i = 0; i < int(sizeof(Desc) / 16); ++i) raw[i] = q[i];
-    Desc d;
-    __builtin_memcpy(&d, raw, sizeof(Desc));
+    const Desc d = load_desc(a, idx);
     if (STAGE) {
         switch (kind_levels(d.kind)) {
             case 1: run_realign<1>(d, a); break;
