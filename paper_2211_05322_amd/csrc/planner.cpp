@@ -434,8 +434,6 @@ int64_t auto_chunk_bytes(int64_t bytes_read) {
     return c;
 }
 
-}  // namespace
-
 // Row-gather lowering of one group (see desc.h).  Returns false, emitting
 // nothing, when the group does not qualify; its tasks then take the
 // per-task path.
@@ -735,6 +733,8 @@ bool lower_gather_unaligned(Plan &p, const std::vector<size_t> &group, int64_t c
     p.gather_u_fanout = std::max(p.gather_u_fanout, nfan);
     return true;
 }
+
+}  // namespace
 
 void lower(Plan &p) {
     const int nd = p.ndim;
