@@ -128,8 +128,10 @@ typedef struct {
  * Errors: EINVAL for a malformed spec, spec length != ndim, an axis outside the
  * mesh or used twice, ndim or mesh_ndim outside 1..8, a negative dimension, a
  * mesh axis < 1, NULL shape/mesh/spec/out; EUNSUPPORTED when the two meshes
- * together have more than RESHARD_MAX_BUFFERS devices; ENOMEM on allocation
- * failure.  *out is set to NULL on error.
+ * together have more than RESHARD_MAX_BUFFERS devices, or the plan would need
+ * more than 2^24 unit tasks or 2^24 workgroup chunks (automatic chunk sizes
+ * grow with the tensor to stay well below; an explicit tuning.chunk_bytes can
+ * exceed it); ENOMEM on allocation failure.  *out is set to NULL on error.
  */
 reshard_status_t reshard_plan(int ndim, const int64_t *shape, reshard_dtype_t dtype,
                               int src_mesh_ndim, const int64_t *src_mesh, const char *src_spec,

@@ -428,9 +428,12 @@ void split_emit(Plan &p, Piece pc, int32_t src_buf, int64_t fan_off, int64_t nfa
 }
 
 int64_t auto_chunk_bytes(int64_t bytes_read) {
-    // Enough chunks to fill 256 CUs many times over, 4 KiB .. 16 KiB each.
+    // Enough chunks to fill 256 CUs many times over, 4 KiB .. 16 KiB each;
+    // past 64 GiB, larger chunks keep the table within a quarter of the
+    // chunk limit.
     int64_t c = 4096;
     while (c < 16384 && bytes_read / (2 * c) >= 4096) c *= 2;
+    while (bytes_read / c > int64_t(kMaxDescs / 4)) c *= 2;
     return c;
 }
 

@@ -275,6 +275,19 @@ def test_plan_error_ndim_and_nulls():
     assert lib.reshard_plan_upload(empty.handle) == B.RESHARD_OK
 
 
+def test_default_chunking_scales_past_the_chunk_limit():
+    # 300 GiB of unique bytes: 16 KiB chunks would exceed the 2^24-chunk
+    # table; automatic chunking grows instead (plan only, no data)
+    p = plan_of((300 << 30,), "uint8", (1,), "R", (2,), "S^0")
+    st = B.reshard_plan_stats(p)
+    assert st["bytes_read"] == 300 << 30
+    assert st["n_descriptors"] <= 1 << 22
+    # an explicitly tiny chunk on a large tensor is refused, not truncated
+    with pytest.raises(B.ReshardError) as e:
+        plan_of((1 << 33,), "uint8", (1,), "R", (1,), "R", chunk_bytes=256)
+    assert e.value.status == B.RESHARD_EUNSUPPORTED and "2^24" in str(e.value)
+
+
 def test_query_errors():
     p = plan_of((4, 4), "float16", (2,), "S^0R", (2,), "RS^0")
     lib = B.load()
