@@ -2,7 +2,8 @@
 
 Pins (against facts, not the oracle's own formula): with no communication
 both schedules take (M + S - 1)(f + b), the classic 1F1B makespan, and are
-equal (Section 4); the warm-up counts set the peak live activations, and
+equal (Section 4); one micro-batch takes S f + (S - 1) c_f + S b + (S - 1)
+c_b (down and back up); one stage takes M (f + b) whatever the transfers; the warm-up counts set the peak live activations, and
 eager-1F1B adds at most #stages of them per stage (Section 4, Table 1
 discussion); communication can only lengthen an iteration; eager-1F1B is
 never slower than 1F1B in these settings.  Parity: the library's simulator
@@ -23,6 +24,25 @@ def test_no_communication_closed_form(S, M, eager):
     f, b = 1.0, 2.0
     lat, _ = P.simulate(S, M, eager, f, b, 0.0, 0.0)
     assert lat == (M + S - 1) * (f + b)
+
+
+@pytest.mark.parametrize("S", [1, 2, 3, 7])
+@pytest.mark.parametrize("eager", [0, 1])
+@pytest.mark.parametrize("serial", [True, False])
+def test_single_microbatch_closed_form(S, eager, serial):
+    # one micro-batch goes down the pipeline and back: every forward, every
+    # backward and one transfer per stage boundary in each direction
+    f, b, cf, cb = 1.0, 2.5, 0.75, 0.25
+    lat, peak = P.simulate(S, 1, eager, f, b, cf, cb, serial)
+    assert lat == S * f + (S - 1) * cf + S * b + (S - 1) * cb
+    assert peak == [1] * S
+
+
+@pytest.mark.parametrize("M", [1, 4, 9])
+@pytest.mark.parametrize("eager", [0, 1])
+def test_single_stage_ignores_transfer_cost(M, eager):
+    lat, _ = P.simulate(1, M, eager, 1.0, 2.0, 5.0, 7.0)
+    assert lat == M * 3.0
 
 
 @pytest.mark.parametrize("S,M", [(2, 8), (4, 4), (4, 13), (6, 24)])
