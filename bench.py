@@ -61,8 +61,6 @@ def measured_traffic(key):
 
 def cpu_baseline(w, src_dev, budget_s):
     """The numpy oracle on host cores, on the same workload (bounded repeat count)."""
-    import numpy as np
-
     import oracle
     from paper_2211_05322_amd.workloads import as_numpy_bits
 
