@@ -482,11 +482,10 @@ __device__ __forceinline__ void stage_segments(const Desc &d, const RS_CONST KAr
     uint32_t *sst = reinterpret_cast<uint32_t *>(rs_lds + 8u * kMaxSegs);
     const RS_CONST Seg *segs = (const RS_CONST Seg *)(a->segs + d.pad[0]);
     for (uint32_t g = threadIdx.x; g < d.pad[1]; g += blockDim.x) {
-        const Seg sg = {segs[g].src_base, {segs[g].ss[0], segs[g].ss[1], segs[g].ss[2]}, segs[g].buf};
-        sp[g] = uint64_t(a->ptr[sg.buf]) + sg.src_base;
-        sst[3 * g] = sg.ss[0];
-        sst[3 * g + 1] = sg.ss[1];
-        sst[3 * g + 2] = sg.ss[2];
+        sp[g] = uint64_t(a->ptr[segs[g].buf]) + segs[g].src_base;
+        sst[3 * g] = segs[g].ss[0];
+        sst[3 * g + 1] = segs[g].ss[1];
+        sst[3 * g + 2] = segs[g].ss[2];
     }
 }
 
@@ -708,7 +707,7 @@ __device__ __forceinline__ void run_gather_u(const Desc &d, const RS_CONST KArgs
         if (has1) uslot_load<L>(d, sp, sst, scol, c1, s1);
         const u32x4 o0 = uslot_compose(s0, c0);
         const u32x4 o1 = has1 ? uslot_compose(s1, c1) : o0;
-        if (RF >= 1 && RF <= 4) {
+        if constexpr (RF >= 1 && RF <= 4) {
 #pragma unroll
             for (uint32_t r = 0; r < nr; ++r)
                 uslot_store((RS_GLOBAL unsigned char *)a->ptr[a->nsrc + uint32_t(fan[r])] + d.dst_base + c0, o0, s0, c0);
@@ -718,8 +717,15 @@ __device__ __forceinline__ void run_gather_u(const Desc &d, const RS_CONST KArgs
                     uslot_store((RS_GLOBAL unsigned char *)a->ptr[a->nsrc + uint32_t(fan[r])] + d.dst_base + c1, o1, s1,
                                 c1);
             }
-        } else {
+        } else if constexpr (RF > 4) {
 #pragma unroll
+            for (uint32_t r = 0; r < nr; ++r) {
+                RS_GLOBAL unsigned char *dst =
+                    (RS_GLOBAL unsigned char *)a->ptr[a->nsrc + uint32_t(fan[r])] + d.dst_base;
+                uslot_store(dst + c0, o0, s0, c0);
+                if (has1) uslot_store(dst + c1, o1, s1, c1);
+            }
+        } else {  // runtime receiver count
             for (uint32_t r = 0; r < nr; ++r) {
                 RS_GLOBAL unsigned char *dst =
                     (RS_GLOBAL unsigned char *)a->ptr[a->nsrc + uint32_t(fan[r])] + d.dst_base;

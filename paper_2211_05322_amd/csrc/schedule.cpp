@@ -174,7 +174,7 @@ struct Dfs {
 };
 
 Sched dfs(const std::vector<STask> &ts, int nhosts, int64_t max_nodes, int64_t *nodes_out) {
-    Dfs d{ts, nhosts, max_nodes};
+    Dfs d{ts, nhosts, max_nodes, 0, {}, {}, {}, {}, {}, {}, {}};
     const size_t n = ts.size();
     d.cls.assign(n, 0);
     for (size_t i = 0; i < n; ++i) {
