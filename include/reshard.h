@@ -162,9 +162,12 @@ reshard_status_t reshard_plan_ex(int ndim, const int64_t *shape, reshard_dtype_t
  * The first call on a device uploads the descriptor table to memory the plan
  * owns (one hipMalloc + synchronous copies) unless reshard_plan_upload did;
  * later calls only launch, so they can be captured into a HIP graph.  A plan
- * may be executed any number of times, on any stream; calls on different
- * streams that write the same destination buffers race, as any two kernels
- * would.
+ * may be executed any number of times, on any stream, from any number of
+ * host threads at once (the first upload on a device is serialised by the
+ * plan's lock); calls on different streams that write the same destination
+ * buffers race, as any two kernels would.  Destroying a plan while another
+ * thread still uses it, or before its launched kernels have finished, is the
+ * caller's error.
  *
  * Errors: EINVAL for NULL plan or pointer arrays, a NULL or misaligned buffer
  * for a non-empty shard; ENOMEM if the table upload cannot allocate; EHIP if a

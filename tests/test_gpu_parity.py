@@ -438,3 +438,44 @@ def test_graph_capture_and_replay(case):
         for k, (d, w) in enumerate(zip(dst, want)):
             assert np.array_equal(as_numpy_bits(d), w), f"replay {rep} destination {k}"
     del g
+
+
+# ----------------------------------------------------- concurrent callers
+
+def test_concurrent_executes_share_one_plan():
+    """Four host threads call reshard_execute on one fresh plan at once, each
+    on its own stream and destination buffers: the table upload happens once
+    (under the plan's lock) and every output is bit-exact."""
+    import threading
+
+    shape, dt, sm, ss, dm, ds = (4, 64, 1024), "float16", (4, 8), "RRS^{01}", (4, 8), "RS^1R"
+    _say("concurrent executes")
+    x = rand_bits(shape, dt, 77)
+    xs = oracle.shard(as_numpy_bits(x), sm, ss)
+    want = oracle.reshard(xs, shape, sm, ss, dm, ds)
+    p = B.reshard_plan(shape, dt, sm, ss, dm, ds)
+    src = [torch.from_numpy(a.view("i2").copy()).cuda() for a in xs]
+    outs = [[torch.full(w.shape, -1, dtype=torch.int16, device="cuda") for w in want] for _ in range(4)]
+    streams = [torch.cuda.Stream() for _ in range(4)]
+    torch.cuda.synchronize()
+    errors = []
+    start = threading.Barrier(4)
+
+    def worker(i):
+        try:
+            start.wait()
+            for _ in range(3):
+                B.reshard_execute(p, src, outs[i], stream=streams[i])
+        except Exception as e:  # reported below
+            errors.append(e)
+
+    threads = [threading.Thread(target=worker, args=(i,)) for i in range(4)]
+    for t in threads:
+        t.start()
+    for t in threads:
+        t.join()
+    torch.cuda.synchronize()
+    assert not errors, errors
+    for i in range(4):
+        for k, (d, w) in enumerate(zip(outs[i], want)):
+            assert np.array_equal(d.cpu().numpy().view(np.uint16), w), f"thread {i} destination {k}"
