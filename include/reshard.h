@@ -121,7 +121,7 @@ typedef struct {
  * Host only, thread-safe, no HIP call.  Computes per-device shard boxes, the
  * unit tasks (non-empty intersections of source and destination shards, each
  * with its owners and its receivers; Section 2.2 and the appendix), the
- * sender of each (flags), and the descriptor table the kernel runs from.
+ * sender of each (flags), and the descriptor table the kernels run from.
  * The source and destination meshes are disjoint sets of buffers (Section 2.2).
  *
  * On success *out owns a new plan (free with reshard_plan_destroy).
@@ -247,7 +247,7 @@ reshard_status_t reshard_plan_unit_task(const reshard_plan_t *plan, int64_t inde
 
 /*
  * Run the plan's descriptor table on HOST memory with a plain loop: the same
- * table, index arithmetic and fan-out the kernel uses, so the lowering can be
+ * table, index arithmetic and fan-out the kernels use, so the lowering can be
  * checked on a machine without a GPU.  Never called by reshard_execute.
  * src_ptrs/dst_ptrs are host pointers with the layout described above.
  * EINVAL for NULL arguments or a NULL buffer of a non-empty shard.

@@ -1,5 +1,5 @@
 // capi.cpp -- C ABI of libreshard.so: planning, queries, host interpreter.
-// reshard_execute and the kernel live in execute.hip.
+// reshard_execute and the kernels live in execute.hip.
 #include <algorithm>
 #include <cstring>
 #include <new>

@@ -1,4 +1,4 @@
-// desc.h -- descriptor table the resharding kernel runs from.
+// desc.h -- descriptor table the resharding kernels run from.
 //
 // One descriptor is one workgroup's chunk of work: a range of W-byte vectors
 // inside a "piece", where a piece is part of one unit task's slice seen as
