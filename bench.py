@@ -22,6 +22,7 @@ import argparse
 import hashlib
 import json
 import os
+import re
 import statistics
 import sys
 import time
@@ -36,10 +37,15 @@ KERNEL_SOURCES = [os.path.join(ROOT, "paper_2211_05322_amd", "csrc", f) for f in
 
 
 def kernel_hash():
+    """Hash of the kernel and lowering code, comments and blank space removed
+    (a comment edit does not invalidate recorded counter traffic)."""
     h = hashlib.sha256()
     for f in KERNEL_SOURCES:
-        with open(f, "rb") as fh:
-            h.update(fh.read())
+        with open(f) as fh:
+            text = fh.read()
+        text = re.sub(r"/\*.*?\*/", " ", text, flags=re.S)
+        text = re.sub(r"//[^\n]*", " ", text)
+        h.update(" ".join(text.split()).encode())
     return h.hexdigest()[:16]
 
 
