@@ -514,3 +514,14 @@ def test_fuzz_lowering_flags_and_tunings(case):
     _say(f"lowering fuzz {case}")
     got, want = run_gpu(shape, dt, sm, ss, dm, ds, rand_bits(shape, dt, zlib.crc32(repr(case).encode())), **kw)
     assert_same(got, want)
+
+
+@pytest.mark.parametrize("dt", ["bfloat16", "int16", "int32", "int64"])
+def test_other_element_types(dt):
+    """The kernels see only the element size: bf16 and the integer types go
+    through the same paths bit for bit (row gather and realignment cases)."""
+    for shape, sm, ss, dm, ds in (((2, 16, 512), (4, 8), "RRS^{01}", (4, 8), "RS^1R"),
+                                  ((3, 40, 333), (2, 2), "RS^0S^1", (3,), "RRS^0")):
+        _say(f"dtype {dt} {shape}")
+        got, want = run_gpu(shape, dt, sm, ss, dm, ds, rand_bits(shape, dt, 31))
+        assert_same(got, want)
