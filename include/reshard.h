@@ -7,9 +7,10 @@
  * on a disjoint destination mesh under spec X_B.  The library decomposes the
  * task into unit communication tasks (one per unique data slice, Section 2.2
  * and the appendix decomposition), picks one sender per slice among the
- * source replicas (Section 3.2), and moves every slice with one fused HIP
- * kernel that reads it once and writes it to every receiver (the broadcast
- * strategy of Section 3.1: one sender, all receivers).
+ * source replicas (Section 3.2), and moves every slice with fused HIP
+ * kernels (one launch per kind of chunk the plan holds) that read it once
+ * and write it to every receiver (the broadcast strategy of Section 3.1:
+ * one sender, all receivers).
  *
  * On one GPU every mesh "device" is a separate buffer in the GPU's memory.
  *
@@ -79,14 +80,16 @@ typedef enum {
                                       funnel-shifted in registers). */
 
 #define RESHARD_NO_GATHER 0x100u   /* copy every unit task separately (default: tasks that share
-                                      a receiver set and cut its rows into equal 16-byte-aligned
-                                      column segments are written row by row, one workgroup
-                                      gathering whole destination rows from their senders). */
+                                      a receiver set and cut its rows into column segments --
+                                      equal and 16-byte aligned, or of any width of at least 16
+                                      bytes over contiguous rows -- are written together, one
+                                      workgroup gathering destination rows or 16-byte slots
+                                      from all their senders). */
 
 /* Comparison strategies (Section 3.1), for measuring what broadcast saves; at
  * most one.  Both read every slice once per receiver (R x the bytes of D) and
- * copy rows directly (no realignment path).  Default: broadcast, one read and
- * one write per receiver in one launch. */
+ * copy rows directly (no row gather, no realignment path).  Default:
+ * broadcast, one read and one write per receiver. */
 #define RESHARD_STRATEGY_SENDRECV 0x20u   /* the sender's slice is re-read for each receiver */
 #define RESHARD_STRATEGY_ALLGATHER 0x40u  /* send/recv + all-gather: chunks go round-robin to the
                                              receivers, then (second launch) each receiver pulls
@@ -100,12 +103,13 @@ typedef enum {
 /* Optional tuning of the lowering; zero fields take the defaults. */
 typedef struct {
     int64_t chunk_bytes;    /* source bytes per workgroup chunk (default: 4..16 KiB, sized
-                               so a large plan has >= 4096 chunks); whole vectors */
+                               so a large plan has >= 4096 chunks, larger past 64 GiB of
+                               unique data); whole vectors */
     int32_t block_threads;  /* threads per workgroup: 64, 128, 256, 512 or 1024 (default 256) */
     int32_t max_wgs_per_cu; /* cap on resident workgroups per CU, 2..32, enforced by reserving
                                LDS per workgroup; 0 = default, chosen per kernel from its
                                fan-out (direct chunks: 16 waves per CU at fan-out <= 2, 12
-                               above; row-gather chunks: 64 / fan-out waves, at least 8;
+                               above; both row-gather kinds: 64 / fan-out waves, at least 8;
                                never below 2 workgroups); -1 = no cap */
     int32_t gather_band;    /* row-gather chunks: column segments per band (>= 0); the chunks
                                of a row group cover one band of the destination rows after
@@ -148,6 +152,16 @@ reshard_status_t reshard_plan_ex(int ndim, const int64_t *shape, reshard_dtype_t
                                  reshard_plan_t **out);
 
 /*
+ * Upload the plan's descriptor, receiver and segment tables to the current
+ * HIP device (one hipMalloc + synchronous copies; nothing if already done
+ * on that device).  After it, reshard_execute on that device allocates and
+ * copies nothing, so it can run under HIP graph capture.  Errors: EINVAL
+ * for a NULL plan, ENOMEM if the allocation fails, EHIP if a HIP call
+ * fails.
+ */
+reshard_status_t reshard_plan_upload(const reshard_plan_t *plan);
+
+/*
  * Run the plan: fill every destination buffer from the source buffers.
  *
  * src_ptrs[k] (k < number of source devices) and dst_ptrs[k] (k < number of
@@ -173,16 +187,6 @@ reshard_status_t reshard_plan_ex(int ndim, const int64_t *shape, reshard_dtype_t
  * for a non-empty shard; ENOMEM if the table upload cannot allocate; EHIP if a
  * HIP call or the launch fails.
  */
-/*
- * Upload the plan's descriptor, receiver and segment tables to the current
- * HIP device (one hipMalloc + synchronous copies; nothing if already done
- * on that device).  After it, reshard_execute on that device allocates and
- * copies nothing, so it can run under HIP graph capture.  Errors: EINVAL
- * for a NULL plan, ENOMEM if the allocation fails, EHIP if a HIP call
- * fails.
- */
-reshard_status_t reshard_plan_upload(const reshard_plan_t *plan);
-
 reshard_status_t reshard_execute(const reshard_plan_t *plan, void *const *src_ptrs,
                                  void *const *dst_ptrs, void *stream);
 
@@ -250,7 +254,9 @@ reshard_status_t reshard_plan_unit_task(const reshard_plan_t *plan, int64_t inde
  * table, index arithmetic and fan-out the kernels use, so the lowering can be
  * checked on a machine without a GPU.  Never called by reshard_execute.
  * src_ptrs/dst_ptrs are host pointers with the layout described above.
- * EINVAL for NULL arguments or a NULL buffer of a non-empty shard.
+ * EINVAL for NULL arguments or a NULL buffer of a non-empty shard, and (text
+ * starting "internal:") when a chunk would touch bytes outside its shard --
+ * a lowering error the kernels would turn into a fault.
  */
 reshard_status_t reshard_debug_execute_host(const reshard_plan_t *plan, void *const *src_ptrs,
                                             void *const *dst_ptrs);
