@@ -598,12 +598,14 @@ bool lower_gather_group(Plan &p, const std::vector<size_t> &group, int64_t chunk
 }
 
 // Unaligned row gather of one group (see desc.h): segments of any widths of
-// at least 16 bytes tiling the destination row, destination rows contiguous.
-// Returns false, emitting nothing, when the group does not qualify.
+// at least 16 bytes tiling the destination row (one segment per row too,
+// when its rows are in different 16-byte phases on the two sides),
+// destination rows contiguous.  Returns false, emitting nothing, when the
+// group does not qualify.
 bool lower_gather_unaligned(Plan &p, const std::vector<size_t> &group, int64_t chunk_bytes, std::vector<Desc> &out) {
     const int nd = p.ndim;
     const int64_t es = p.es;
-    if (nd < 1 || group.size() < 2 || group.size() > kMaxSegs) return false;
+    if (nd < 1 || group.empty() || group.size() > kMaxSegs) return false;
     std::vector<size_t> g(group);
     std::sort(g.begin(), g.end(), [&](size_t a, size_t b) { return p.tasks[a].lo[nd - 1] < p.tasks[b].lo[nd - 1]; });
     const UnitTask &t0 = p.tasks[g[0]];
@@ -683,6 +685,15 @@ bool lower_gather_unaligned(Plan &p, const std::vector<size_t> &group, int64_t c
     }
     uint64_t d0 = 0;  // the group's first byte in the receivers' buffers
     for (int d = 0; d < nd - 1; ++d) d0 += uint64_t((t0.lo[d] - dlo[d]) * str_d[d]);
+    if (ns == 1) {
+        // One sender per row: only where the per-task lowering would need the
+        // realignment kernel (the two sides' rows in different 16-byte
+        // phases); slots of the contiguous destination rows then keep every
+        // cache line within one workgroup.
+        bool same_phase = row_bytes % 16 == 0 && (seg[0].src_base - d0) % 16 == 0;
+        for (const auto &l : lv) same_phase = same_phase && l.ss[0] % 16 == 0;
+        if (same_phase) return false;
+    }
     const uint64_t total = rows * uint64_t(row_bytes);
     const int levels = std::max<int>(1, int(lv.size()));
     Desc d{};

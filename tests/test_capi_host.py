@@ -401,6 +401,10 @@ UNALIGNED_GATHER_CASES = [
     ((2, 5, 8, 12), "float64", (2, 2), "RRRS^{01}", (2,), "RRRR"),      # 24-byte segments
     ((2, 8, 650), "float16", (1, 4), "RRS^1", (3, 4), "RRR"),           # fan-out 12: runtime receiver loop
     ((3, 16, 1000), "uint8", (5,), "RRS^0", (2, 5), "RRR"),             # fan-out 10, 200-byte segments
+    # one sender per row, the two sides' rows in different 16-byte phases
+    ((8, 64, 1230), "float16", (1,), "RRR", (4,), "RRS^0"),             # 616/614-byte rows from one source
+    ((7, 130), "float64", (2,), "S^0R", (3, 2), "RS^0"),                # fan-out 2, 344/352-byte rows
+    ((5, 1000), "uint8", (1,), "RR", (3,), "RS^0"),                     # byte rows of 334/333
 ]
 
 
@@ -410,7 +414,7 @@ def test_host_unaligned_gather(case, chunk):
     shape, dt, sm, ss, dm, ds = case
     p = plan_of(shape, dt, sm, ss, dm, ds, chunk_bytes=chunk)
     assert B.reshard_plan_unaligned_gather_chunks(p) > 0, "case should take the unaligned row gather"
-    assert B.reshard_plan_gather_chunks(p) == 0
+    assert B.reshard_plan_gather_chunks(p) == 0 and B.reshard_plan_realign_chunks(p) == 0
     host_case(shape, dt, sm, ss, dm, ds, chunk_bytes=chunk)
     q = plan_of(shape, dt, sm, ss, dm, ds, flags=B.RESHARD_NO_GATHER)
     assert B.reshard_plan_unaligned_gather_chunks(q) == 0
@@ -418,10 +422,12 @@ def test_host_unaligned_gather(case, chunk):
 
 
 def test_unaligned_gather_declines():
-    # segments under 16 bytes, or destination rows that are not contiguous:
+    # segments under 16 bytes, destination rows that are not contiguous, or
+    # one sender per row with both sides in the same 16-byte phase:
     # per-task chunks instead
     for case in (((4, 8, 40), "float16", (8,), "RRS^0", (2,), "S^0RR"),
-                 ((6, 10, 300), "float16", (2, 3), "RS^0S^1", (2,), "RRS^0")):
+                 ((6, 10, 300), "float16", (2, 3), "RS^0S^1", (2,), "RRS^0"),
+                 ((8, 64, 1024), "float16", (1,), "RRR", (4,), "RRS^0")):
         p = plan_of(*case)
         assert B.reshard_plan_unaligned_gather_chunks(p) == 0
         host_case(*case)
