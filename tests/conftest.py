@@ -15,7 +15,7 @@ def pytest_configure(config):
 
 @pytest.fixture(scope="session")
 def gpu_lib():
-    """The built HIP library on a GPU machine; errors loudly when either is missing."""
+    """The built HIP library on a machine with a GPU; errors loudly when either is missing."""
     import torch
 
     if not torch.cuda.is_available():
