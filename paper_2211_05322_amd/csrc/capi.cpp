@@ -8,6 +8,7 @@
 
 #include "../../include/reshard.h"
 #include "planner.hpp"
+#include "status.hpp"
 
 namespace rs {
 // Defined in execute.hip: frees the plan's device table (if any).
@@ -15,8 +16,21 @@ void release_device_table(const Plan &p);
 
 thread_local std::string g_last_error;
 
-reshard_status_t fail(reshard_status_t st, const std::string &msg) {
-    g_last_error = msg;
+reshard_status_t fail(reshard_status_t st, const std::string &msg) noexcept {
+    try {
+        g_last_error = msg;
+    } catch (...) {
+        g_last_error.clear();
+    }
+    return st;
+}
+
+reshard_status_t fail(reshard_status_t st, const char *msg) noexcept {
+    try {
+        g_last_error = msg;
+    } catch (...) {
+        g_last_error.clear();
+    }
     return st;
 }
 }  // namespace rs
@@ -155,47 +169,58 @@ reshard_status_t reshard_plan(int ndim, const int64_t *shape, reshard_dtype_t dt
                               const int64_t *src_mesh, const char *src_spec, int dst_mesh_ndim,
                               const int64_t *dst_mesh, const char *dst_spec, unsigned flags,
                               reshard_plan_t **out) {
-    return make_plan(ndim, shape, dtype, src_mesh_ndim, src_mesh, src_spec, dst_mesh_ndim, dst_mesh, dst_spec,
-                     flags, nullptr, out);
+    return rs::guarded([&]() -> reshard_status_t {
+        return make_plan(ndim, shape, dtype, src_mesh_ndim, src_mesh, src_spec, dst_mesh_ndim, dst_mesh, dst_spec,
+                         flags, nullptr, out);
+    });
 }
 
 reshard_status_t reshard_plan_ex(int ndim, const int64_t *shape, reshard_dtype_t dtype, int src_mesh_ndim,
                                  const int64_t *src_mesh, const char *src_spec, int dst_mesh_ndim,
                                  const int64_t *dst_mesh, const char *dst_spec, unsigned flags,
                                  const reshard_tuning_t *tuning, reshard_plan_t **out) {
-    return make_plan(ndim, shape, dtype, src_mesh_ndim, src_mesh, src_spec, dst_mesh_ndim, dst_mesh, dst_spec,
-                     flags, tuning, out);
+    return rs::guarded([&]() -> reshard_status_t {
+        return make_plan(ndim, shape, dtype, src_mesh_ndim, src_mesh, src_spec, dst_mesh_ndim, dst_mesh, dst_spec,
+                         flags, tuning, out);
+    });
 }
 
 void reshard_plan_destroy(reshard_plan_t *plan) {
     if (!plan) return;
     rs::Plan *p = reinterpret_cast<rs::Plan *>(plan);
-    rs::release_device_table(*p);
+    try {
+        rs::release_device_table(*p);
+    } catch (...) {  // (the lock cannot be taken: nothing else to release)
+    }
     delete p;
 }
 
 reshard_status_t reshard_plan_local_shape(const reshard_plan_t *plan, int side, int64_t device,
                                           int64_t *shape_out) {
-    const rs::Plan *p = as_plan(plan);
-    if (!p || !shape_out) return fail(RESHARD_EINVAL, "NULL plan or shape_out");
-    if (side != 0 && side != 1) return fail(RESHARD_EINVAL, "side must be 0 (source) or 1 (destination)");
-    const int64_t n = side == 0 ? p->src.ndev : p->dst.ndev;
-    if (device < 0 || device >= n)
-        return fail(RESHARD_EINVAL, "device " + std::to_string(device) + " outside 0.." + std::to_string(n - 1));
-    rs::local_shape(*p, side, device, shape_out);
-    return RESHARD_OK;
+    return rs::guarded([&]() -> reshard_status_t {
+        const rs::Plan *p = as_plan(plan);
+        if (!p || !shape_out) return fail(RESHARD_EINVAL, "NULL plan or shape_out");
+        if (side != 0 && side != 1) return fail(RESHARD_EINVAL, "side must be 0 (source) or 1 (destination)");
+        const int64_t n = side == 0 ? p->src.ndev : p->dst.ndev;
+        if (device < 0 || device >= n)
+            return fail(RESHARD_EINVAL, "device " + std::to_string(device) + " outside 0.." + std::to_string(n - 1));
+        rs::local_shape(*p, side, device, shape_out);
+        return RESHARD_OK;
+    });
 }
 
 reshard_status_t reshard_plan_stats(const reshard_plan_t *plan, int64_t *bytes_read, int64_t *bytes_written,
                                     int64_t *n_unit_tasks, int64_t *n_descriptors, int64_t *max_fanout) {
-    const rs::Plan *p = as_plan(plan);
-    if (!p) return fail(RESHARD_EINVAL, "NULL plan");
-    if (bytes_read) *bytes_read = p->bytes_read;
-    if (bytes_written) *bytes_written = p->bytes_written;
-    if (n_unit_tasks) *n_unit_tasks = int64_t(p->tasks.size());
-    if (n_descriptors) *n_descriptors = int64_t(p->descs.size());
-    if (max_fanout) *max_fanout = p->max_fanout;
-    return RESHARD_OK;
+    return rs::guarded([&]() -> reshard_status_t {
+        const rs::Plan *p = as_plan(plan);
+        if (!p) return fail(RESHARD_EINVAL, "NULL plan");
+        if (bytes_read) *bytes_read = p->bytes_read;
+        if (bytes_written) *bytes_written = p->bytes_written;
+        if (n_unit_tasks) *n_unit_tasks = int64_t(p->tasks.size());
+        if (n_descriptors) *n_descriptors = int64_t(p->descs.size());
+        if (max_fanout) *max_fanout = p->max_fanout;
+        return RESHARD_OK;
+    });
 }
 
 int64_t reshard_plan_alignment(const reshard_plan_t *plan) {
@@ -228,242 +253,246 @@ reshard_status_t reshard_plan_unit_task(const reshard_plan_t *plan, int64_t inde
                                         int64_t *chosen_sender, int64_t *senders, int64_t senders_cap,
                                         int64_t *n_senders, int64_t *receivers, int64_t receivers_cap,
                                         int64_t *n_receivers) {
-    const rs::Plan *p = as_plan(plan);
-    if (!p || !lo || !hi) return fail(RESHARD_EINVAL, "NULL plan, lo or hi");
-    if (index < 0 || index >= int64_t(p->tasks.size()))
-        return fail(RESHARD_EINVAL, "unit task index " + std::to_string(index) + " out of range");
-    if ((senders_cap > 0 && !senders) || (receivers_cap > 0 && !receivers) || senders_cap < 0 || receivers_cap < 0)
-        return fail(RESHARD_EINVAL, "NULL output array with non-zero capacity");
-    const rs::UnitTask &t = p->tasks[size_t(index)];
-    for (int d = 0; d < p->ndim; ++d) {
-        lo[d] = t.lo[d];
-        hi[d] = t.hi[d];
-    }
-    if (chosen_sender) *chosen_sender = t.sender;
-    const int64_t s0 = p->src.shard_devs_off[t.src_shard], s1 = p->src.shard_devs_off[t.src_shard + 1];
-    for (int64_t k = s0; k < s1 && k - s0 < senders_cap; ++k) senders[k - s0] = p->src.shard_devs[k];
-    if (n_senders) *n_senders = s1 - s0;
-    const int64_t r0 = p->dst.shard_devs_off[t.dst_shard], r1 = p->dst.shard_devs_off[t.dst_shard + 1];
-    for (int64_t k = r0; k < r1 && k - r0 < receivers_cap; ++k) receivers[k - r0] = p->dst.shard_devs[k];
-    if (n_receivers) *n_receivers = r1 - r0;
-    return RESHARD_OK;
+    return rs::guarded([&]() -> reshard_status_t {
+        const rs::Plan *p = as_plan(plan);
+        if (!p || !lo || !hi) return fail(RESHARD_EINVAL, "NULL plan, lo or hi");
+        if (index < 0 || index >= int64_t(p->tasks.size()))
+            return fail(RESHARD_EINVAL, "unit task index " + std::to_string(index) + " out of range");
+        if ((senders_cap > 0 && !senders) || (receivers_cap > 0 && !receivers) || senders_cap < 0 || receivers_cap < 0)
+            return fail(RESHARD_EINVAL, "NULL output array with non-zero capacity");
+        const rs::UnitTask &t = p->tasks[size_t(index)];
+        for (int d = 0; d < p->ndim; ++d) {
+            lo[d] = t.lo[d];
+            hi[d] = t.hi[d];
+        }
+        if (chosen_sender) *chosen_sender = t.sender;
+        const int64_t s0 = p->src.shard_devs_off[t.src_shard], s1 = p->src.shard_devs_off[t.src_shard + 1];
+        for (int64_t k = s0; k < s1 && k - s0 < senders_cap; ++k) senders[k - s0] = p->src.shard_devs[k];
+        if (n_senders) *n_senders = s1 - s0;
+        const int64_t r0 = p->dst.shard_devs_off[t.dst_shard], r1 = p->dst.shard_devs_off[t.dst_shard + 1];
+        for (int64_t k = r0; k < r1 && k - r0 < receivers_cap; ++k) receivers[k - r0] = p->dst.shard_devs[k];
+        if (n_receivers) *n_receivers = r1 - r0;
+        return RESHARD_OK;
+    });
 }
 
 reshard_status_t reshard_debug_execute_host(const reshard_plan_t *plan, void *const *src_ptrs,
                                             void *const *dst_ptrs) {
-    const rs::Plan *p = as_plan(plan);
-    if (!p || !src_ptrs || !dst_ptrs) return fail(RESHARD_EINVAL, "NULL plan or pointer array");
-    for (int64_t k = 0; k < p->src.ndev; ++k)
-        if (p->src_local_numel[k] > 0 && !src_ptrs[k])
-            return fail(RESHARD_EINVAL, "source buffer " + std::to_string(k) + " is NULL but its shard is not empty");
-    for (int64_t k = 0; k < p->dst.ndev; ++k)
-        if (p->dst_local_numel[k] > 0 && !dst_ptrs[k])
-            return fail(RESHARD_EINVAL, "destination buffer " + std::to_string(k) + " is NULL but its shard is not empty");
-    std::vector<uint8_t> lds;
-    for (size_t di = 0; di < p->descs.size(); ++di) {
-        const rs::Desc &d = p->descs[di];
-        const uint32_t w = 1u << rs::kind_log2w(d.kind);
-        const uint32_t levels = rs::kind_levels(d.kind);
-        if (di >= p->n_direct + p->n_gather && di < p->n_direct + p->n_gather + p->n_gather_u) {
-            // unaligned row-gather chunk: the kernel's slot -> pieces arithmetic
-            const uint32_t rb = d.vpr, ns = d.pad[1];
-            if (d.pad[0] + ns > p->segs.size() || ns == 0) return fail(RESHARD_EINVAL, "internal: segment table range");
-            const rs::Seg *sg = &p->segs[d.pad[0]];
-            if (sg[0].col != 0) return fail(RESHARD_EINVAL, "internal: first segment does not start the row");
-            auto find_segment = [&](uint32_t col) {
-                uint32_t g = rs::fastdiv(col, d.batch, d.pad[2]);
-                if (g >= ns) g = ns - 1;
-                while (g > 0 && col < sg[g].col) --g;
-                while (g + 1 < ns && col >= sg[g + 1].col) ++g;
-                return g;
-            };
-            // copy piece [col, col + len) of segment g, row `row`, to out
-            auto piece = [&](uint32_t row, uint32_t g, uint32_t col, uint32_t len, uint8_t *out) -> bool {
-                const uint32_t send = g + 1 < ns ? sg[g + 1].col : rb;
-                if (col < sg[g].col || col + len > send) return false;
-                uint32_t i1 = 0, i2 = 0, i3 = 0;
-                if (levels == 1) rs::row_indices<1>(d, row, i1, i2, i3);
-                else if (levels == 2) rs::row_indices<2>(d, row, i1, i2, i3);
-                else rs::row_indices<3>(d, row, i1, i2, i3);
-                const uint32_t off = i1 * sg[g].ss[0] + i2 * sg[g].ss[1] + i3 * sg[g].ss[2] + (col - sg[g].col);
-                const uint64_t q = sg[g].src_base + off;
-                if (q + len > uint64_t(p->src_local_numel[sg[g].buf] * p->es)) return false;
-                std::memcpy(out, static_cast<const char *>(src_ptrs[sg[g].buf]) + q, len);
-                return true;
-            };
-            for (uint32_t ls = d.v0; ls < d.v1; ++ls) {
-                const uint32_t c0 = 16u * ls;
-                const uint32_t lo = std::max(c0, d.ss[2]), hi = std::min(c0 + 16u, d.src_rel0);
-                if (lo >= hi) continue;
-                uint8_t out[16];
-                const uint32_t t = lo + d.ss[1];
-                const uint32_t dr = rs::fastdiv(t, d.mul_vpr, d.sh_vpr);
-                uint32_t row = d.ss[0] + dr, col = t - dr * rb;
-                uint32_t g = find_segment(col);
-                const uint32_t send = g + 1 < ns ? sg[g + 1].col : rb;
-                const uint32_t e1 = lo + std::min(hi - lo, send - col);
-                if (!piece(row, g, col, e1 - lo, out + (lo - c0)))
-                    return fail(RESHARD_EINVAL, "internal: unaligned gather piece outside its segment or shard");
-                if (e1 < hi) {
-                    if (send == rb) {
-                        ++row;
-                        col = 0;
-                        g = 0;
-                    } else {
-                        col = send;
-                        ++g;
-                    }
-                    if (!piece(row, g, col, hi - e1, out + (e1 - c0)))
+    return rs::guarded([&]() -> reshard_status_t {
+        const rs::Plan *p = as_plan(plan);
+        if (!p || !src_ptrs || !dst_ptrs) return fail(RESHARD_EINVAL, "NULL plan or pointer array");
+        for (int64_t k = 0; k < p->src.ndev; ++k)
+            if (p->src_local_numel[k] > 0 && !src_ptrs[k])
+                return fail(RESHARD_EINVAL, "source buffer " + std::to_string(k) + " is NULL but its shard is not empty");
+        for (int64_t k = 0; k < p->dst.ndev; ++k)
+            if (p->dst_local_numel[k] > 0 && !dst_ptrs[k])
+                return fail(RESHARD_EINVAL, "destination buffer " + std::to_string(k) + " is NULL but its shard is not empty");
+        std::vector<uint8_t> lds;
+        for (size_t di = 0; di < p->descs.size(); ++di) {
+            const rs::Desc &d = p->descs[di];
+            const uint32_t w = 1u << rs::kind_log2w(d.kind);
+            const uint32_t levels = rs::kind_levels(d.kind);
+            if (di >= p->n_direct + p->n_gather && di < p->n_direct + p->n_gather + p->n_gather_u) {
+                // unaligned row-gather chunk: the kernel's slot -> pieces arithmetic
+                const uint32_t rb = d.vpr, ns = d.pad[1];
+                if (d.pad[0] + ns > p->segs.size() || ns == 0) return fail(RESHARD_EINVAL, "internal: segment table range");
+                const rs::Seg *sg = &p->segs[d.pad[0]];
+                if (sg[0].col != 0) return fail(RESHARD_EINVAL, "internal: first segment does not start the row");
+                auto find_segment = [&](uint32_t col) {
+                    uint32_t g = rs::fastdiv(col, d.batch, d.pad[2]);
+                    if (g >= ns) g = ns - 1;
+                    while (g > 0 && col < sg[g].col) --g;
+                    while (g + 1 < ns && col >= sg[g + 1].col) ++g;
+                    return g;
+                };
+                // copy piece [col, col + len) of segment g, row `row`, to out
+                auto piece = [&](uint32_t row, uint32_t g, uint32_t col, uint32_t len, uint8_t *out) -> bool {
+                    const uint32_t send = g + 1 < ns ? sg[g + 1].col : rb;
+                    if (col < sg[g].col || col + len > send) return false;
+                    uint32_t i1 = 0, i2 = 0, i3 = 0;
+                    if (levels == 1) rs::row_indices<1>(d, row, i1, i2, i3);
+                    else if (levels == 2) rs::row_indices<2>(d, row, i1, i2, i3);
+                    else rs::row_indices<3>(d, row, i1, i2, i3);
+                    const uint32_t off = i1 * sg[g].ss[0] + i2 * sg[g].ss[1] + i3 * sg[g].ss[2] + (col - sg[g].col);
+                    const uint64_t q = sg[g].src_base + off;
+                    if (q + len > uint64_t(p->src_local_numel[sg[g].buf] * p->es)) return false;
+                    std::memcpy(out, static_cast<const char *>(src_ptrs[sg[g].buf]) + q, len);
+                    return true;
+                };
+                for (uint32_t ls = d.v0; ls < d.v1; ++ls) {
+                    const uint32_t c0 = 16u * ls;
+                    const uint32_t lo = std::max(c0, d.ss[2]), hi = std::min(c0 + 16u, d.src_rel0);
+                    if (lo >= hi) continue;
+                    uint8_t out[16];
+                    const uint32_t t = lo + d.ss[1];
+                    const uint32_t dr = rs::fastdiv(t, d.mul_vpr, d.sh_vpr);
+                    uint32_t row = d.ss[0] + dr, col = t - dr * rb;
+                    uint32_t g = find_segment(col);
+                    const uint32_t send = g + 1 < ns ? sg[g + 1].col : rb;
+                    const uint32_t e1 = lo + std::min(hi - lo, send - col);
+                    if (!piece(row, g, col, e1 - lo, out + (lo - c0)))
                         return fail(RESHARD_EINVAL, "internal: unaligned gather piece outside its segment or shard");
-                }
-                for (uint32_t r = 0; r < d.nfan; ++r) {
-                    const int32_t dev = p->fan[d.fan_off + r];
-                    if (d.dst_base + hi > uint64_t(p->dst_local_numel[dev] * p->es))
-                        return fail(RESHARD_EINVAL, "internal: unaligned gather store outside its destination shard");
-                    std::memcpy(static_cast<char *>(dst_ptrs[dev]) + d.dst_base + lo, out + (lo - c0), hi - lo);
-                }
-            }
-            continue;
-        }
-        if (di >= p->n_direct && di < p->n_direct + p->n_gather) {
-            // row-gather chunk: the kernel's slot -> (row, segment) arithmetic
-            const uint32_t spr = d.vpr, sps = d.run;
-            if (d.pad[0] + d.pad[1] > p->segs.size()) return fail(RESHARD_EINVAL, "internal: segment table range");
-            for (uint32_t v = d.v0; v < d.v1; ++v) {
-                const uint32_t row = rs::fastdiv(v, d.mul_vpr, d.sh_vpr), j = v - row * spr;
-                const uint32_t g = rs::fastdiv(j, d.batch, d.pad[2]), jj = j - g * sps;
-                if (g >= d.pad[1]) return fail(RESHARD_EINVAL, "internal: segment index out of range");
-                uint32_t i1 = 0, i2 = 0, i3 = 0;
-                if (levels == 1) rs::row_indices<1>(d, row, i1, i2, i3);
-                else if (levels == 2) rs::row_indices<2>(d, row, i1, i2, i3);
-                else rs::row_indices<3>(d, row, i1, i2, i3);
-                const uint32_t dr = i1 * d.ds[0] + i2 * d.ds[1] + i3 * d.ds[2] + 16u * j - d.dst_rel0;
-                const rs::Seg &sg = p->segs[d.pad[0] + g];
-                const uint32_t sr = i1 * sg.ss[0] + i2 * sg.ss[1] + i3 * sg.ss[2] + 16u * jj;
-                if (sg.src_base + sr + 16 > uint64_t(p->src_local_numel[sg.buf] * p->es))
-                    return fail(RESHARD_EINVAL, "internal: gather load outside its source shard");
-                const char *src = static_cast<const char *>(src_ptrs[sg.buf]) + sg.src_base + sr;
-                for (uint32_t r = 0; r < d.nfan; ++r) {
-                    if (d.dst_base + dr + 16 > uint64_t(p->dst_local_numel[p->fan[d.fan_off + r]] * p->es))
-                        return fail(RESHARD_EINVAL, "internal: gather store outside its destination shard");
-                    char *dst = static_cast<char *>(dst_ptrs[p->fan[d.fan_off + r]]) + d.dst_base + dr;
-                    std::memcpy(dst, src, 16);
-                }
-            }
-            continue;
-        }
-        // a source index past the source mesh names a destination buffer
-        // (the all-gather strategy's second phase)
-        const int64_t sbuf = int64_t(d.src_buf);
-        const char *src = static_cast<const char *>(sbuf < p->src.ndev ? src_ptrs[sbuf] : dst_ptrs[sbuf - p->src.ndev]) +
-                          d.src_base;
-        if (rs::kind_realign(d.kind) && !(p->flags & RESHARD_LDS_STAGING)) {
-            // The kernel's shifted-load realignment, same arithmetic: every
-            // loaded word must hold a byte of its row.
-            const uint32_t m = d.vpr, run = d.run, sb = uint32_t(d.src_base), db = uint32_t(d.dst_base);
-            const uint32_t n = (d.v1 - d.v0) * m;
-            auto load_word = [&](const rs::Rel &o, uint32_t sph, int32_t j, uint32_t out[4]) -> bool {
-                const int32_t off = int32_t(o.src - sph + 16u * uint32_t(j));
-                const int64_t rel = int64_t(off) - int64_t(o.src);  // row-relative word start
-                if (rel + 16 <= 0 || rel >= int64_t(run)) return false;
-                if (((sb + uint32_t(off)) & 15u) != 0) return false;
-                uint8_t b[16] = {0};
-                for (int64_t t = 0; t < 16; ++t)
-                    if (rel + t >= 0 && rel + t < int64_t(run)) b[t] = uint8_t(src[int64_t(off) + t]);
-                std::memcpy(out, b, 16);
-                return true;
-            };
-            for (uint32_t i = 0; i < n; ++i) {
-                const uint32_t br = rs::fastdiv(i, d.mul_vpr, d.sh_vpr), k = i - br * m;
-                const rs::Rel o = levels == 1 ? rs::row_offsets<1>(d, d.v0 + br)
-                                  : levels == 2 ? rs::row_offsets<2>(d, d.v0 + br) : rs::row_offsets<3>(d, d.v0 + br);
-                const uint32_t sph = (sb + o.src) & 15u, tph = (db + o.dst) & 15u;
-                const int32_t start = int32_t(16u * k) - int32_t(tph);
-                const int32_t lo = std::max(start, 0), hi = std::min(start + 16, int32_t(run));
-                if (lo >= hi) continue;
-                const int32_t pos = int32_t(sph) + start;
-                const int32_t j0 = pos >> 4;
-                uint32_t w[8] = {0};
-                if (j0 >= 0 && !load_word(o, sph, j0, w)) return fail(RESHARD_EINVAL, "internal: shifted load outside its row");
-                if (16 * (j0 + 1) < int32_t(sph + run) && !load_word(o, sph, j0 + 1, w + 4))
-                    return fail(RESHARD_EINVAL, "internal: shifted load outside its row");
-                const uint32_t sh = uint32_t(pos) & 15u, t4 = sh >> 2, b = sh & 3u;
-                uint32_t v[4];
-                for (uint32_t t = 0; t < 4; ++t) v[t] = rs::align_byte(w[t4 + t + 1], w[t4 + t], b);
-                uint8_t bytes[16];
-                std::memcpy(bytes, v, 16);
-                for (uint32_t r = 0; r < d.nfan; ++r) {
-                    char *dst = static_cast<char *>(dst_ptrs[p->fan[d.fan_off + r]]) + d.dst_base + o.dst;
-                    for (int32_t c = lo; c < hi; ++c) dst[c] = char(bytes[c - start]);
-                }
-            }
-            continue;
-        }
-        if (rs::kind_realign(d.kind)) {
-            // Same staging layout, slot arithmetic and dword funnel shifts as
-            // the kernel's LDS path, with every staging access bounds-checked.
-            const uint32_t m = d.vpr, run = d.run, sb = uint32_t(d.src_base), db = uint32_t(d.dst_base);
-            lds.assign(rs::realign_lds_bytes(d.batch, m), 0);
-            auto row_off = [&](uint32_t row) {
-                return levels == 1 ? rs::row_offsets<1>(d, row)
-                       : levels == 2 ? rs::row_offsets<2>(d, row) : rs::row_offsets<3>(d, row);
-            };
-            for (uint32_t r0 = d.v0; r0 < d.v1; r0 += d.batch) {
-                const uint32_t nb = std::min(d.batch, d.v1 - r0);
-                std::fill(lds.begin(), lds.end(), 0);
-                for (uint32_t i = 0; i < nb * m; ++i) {
-                    const uint32_t br = rs::fastdiv(i, d.mul_vpr, d.sh_vpr), j = i - br * m;
-                    const rs::Rel o = row_off(r0 + br);
-                    const uint32_t ph = (sb + o.src) & 15u;
-                    if (16u * j >= ph + run) continue;
-                    const uint32_t at = rs::kRealignFront + 16u * i;
-                    if (at + 16u > lds.size()) return fail(RESHARD_EINVAL, "internal: staging write out of range");
-                    // the kernel's signed 32-bit word offset; copy only the
-                    // row's bytes of the aligned source word
-                    const int32_t off = int32_t(o.src + 16u * j - ph);
-                    const int64_t wbeg = int64_t(o.src) - ph + 16 * int64_t(j);
-                    if (int64_t(off) != wbeg) return fail(RESHARD_EINVAL, "internal: staging word offset wraps");
-                    if (((sb + uint32_t(off)) & 15u) != 0) return fail(RESHARD_EINVAL, "internal: staging word misaligned");
-                    for (int64_t b = 0; b < 16; ++b) {
-                        const int64_t pos = wbeg + b - int64_t(o.src);  // row-relative
-                        if (pos >= 0 && pos < int64_t(run)) lds[at + b] = uint8_t(src[wbeg + b]);
+                    if (e1 < hi) {
+                        if (send == rb) {
+                            ++row;
+                            col = 0;
+                            g = 0;
+                        } else {
+                            col = send;
+                            ++g;
+                        }
+                        if (!piece(row, g, col, hi - e1, out + (e1 - c0)))
+                            return fail(RESHARD_EINVAL, "internal: unaligned gather piece outside its segment or shard");
+                    }
+                    for (uint32_t r = 0; r < d.nfan; ++r) {
+                        const int32_t dev = p->fan[d.fan_off + r];
+                        if (d.dst_base + hi > uint64_t(p->dst_local_numel[dev] * p->es))
+                            return fail(RESHARD_EINVAL, "internal: unaligned gather store outside its destination shard");
+                        std::memcpy(static_cast<char *>(dst_ptrs[dev]) + d.dst_base + lo, out + (lo - c0), hi - lo);
                     }
                 }
-                for (uint32_t i = 0; i < nb * m; ++i) {
+                continue;
+            }
+            if (di >= p->n_direct && di < p->n_direct + p->n_gather) {
+                // row-gather chunk: the kernel's slot -> (row, segment) arithmetic
+                const uint32_t spr = d.vpr, sps = d.run;
+                if (d.pad[0] + d.pad[1] > p->segs.size()) return fail(RESHARD_EINVAL, "internal: segment table range");
+                for (uint32_t v = d.v0; v < d.v1; ++v) {
+                    const uint32_t row = rs::fastdiv(v, d.mul_vpr, d.sh_vpr), j = v - row * spr;
+                    const uint32_t g = rs::fastdiv(j, d.batch, d.pad[2]), jj = j - g * sps;
+                    if (g >= d.pad[1]) return fail(RESHARD_EINVAL, "internal: segment index out of range");
+                    uint32_t i1 = 0, i2 = 0, i3 = 0;
+                    if (levels == 1) rs::row_indices<1>(d, row, i1, i2, i3);
+                    else if (levels == 2) rs::row_indices<2>(d, row, i1, i2, i3);
+                    else rs::row_indices<3>(d, row, i1, i2, i3);
+                    const uint32_t dr = i1 * d.ds[0] + i2 * d.ds[1] + i3 * d.ds[2] + 16u * j - d.dst_rel0;
+                    const rs::Seg &sg = p->segs[d.pad[0] + g];
+                    const uint32_t sr = i1 * sg.ss[0] + i2 * sg.ss[1] + i3 * sg.ss[2] + 16u * jj;
+                    if (sg.src_base + sr + 16 > uint64_t(p->src_local_numel[sg.buf] * p->es))
+                        return fail(RESHARD_EINVAL, "internal: gather load outside its source shard");
+                    const char *src = static_cast<const char *>(src_ptrs[sg.buf]) + sg.src_base + sr;
+                    for (uint32_t r = 0; r < d.nfan; ++r) {
+                        if (d.dst_base + dr + 16 > uint64_t(p->dst_local_numel[p->fan[d.fan_off + r]] * p->es))
+                            return fail(RESHARD_EINVAL, "internal: gather store outside its destination shard");
+                        char *dst = static_cast<char *>(dst_ptrs[p->fan[d.fan_off + r]]) + d.dst_base + dr;
+                        std::memcpy(dst, src, 16);
+                    }
+                }
+                continue;
+            }
+            // a source index past the source mesh names a destination buffer
+            // (the all-gather strategy's second phase)
+            const int64_t sbuf = int64_t(d.src_buf);
+            const char *src = static_cast<const char *>(sbuf < p->src.ndev ? src_ptrs[sbuf] : dst_ptrs[sbuf - p->src.ndev]) +
+                              d.src_base;
+            if (rs::kind_realign(d.kind) && !(p->flags & RESHARD_LDS_STAGING)) {
+                // The kernel's shifted-load realignment, same arithmetic: every
+                // loaded word must hold a byte of its row.
+                const uint32_t m = d.vpr, run = d.run, sb = uint32_t(d.src_base), db = uint32_t(d.dst_base);
+                const uint32_t n = (d.v1 - d.v0) * m;
+                auto load_word = [&](const rs::Rel &o, uint32_t sph, int32_t j, uint32_t out[4]) -> bool {
+                    const int32_t off = int32_t(o.src - sph + 16u * uint32_t(j));
+                    const int64_t rel = int64_t(off) - int64_t(o.src);  // row-relative word start
+                    if (rel + 16 <= 0 || rel >= int64_t(run)) return false;
+                    if (((sb + uint32_t(off)) & 15u) != 0) return false;
+                    uint8_t b[16] = {0};
+                    for (int64_t t = 0; t < 16; ++t)
+                        if (rel + t >= 0 && rel + t < int64_t(run)) b[t] = uint8_t(src[int64_t(off) + t]);
+                    std::memcpy(out, b, 16);
+                    return true;
+                };
+                for (uint32_t i = 0; i < n; ++i) {
                     const uint32_t br = rs::fastdiv(i, d.mul_vpr, d.sh_vpr), k = i - br * m;
-                    const rs::Rel o = row_off(r0 + br);
+                    const rs::Rel o = levels == 1 ? rs::row_offsets<1>(d, d.v0 + br)
+                                      : levels == 2 ? rs::row_offsets<2>(d, d.v0 + br) : rs::row_offsets<3>(d, d.v0 + br);
                     const uint32_t sph = (sb + o.src) & 15u, tph = (db + o.dst) & 15u;
                     const int32_t start = int32_t(16u * k) - int32_t(tph);
                     const int32_t lo = std::max(start, 0), hi = std::min(start + 16, int32_t(run));
                     if (lo >= hi) continue;
-                    const uint32_t q = rs::kRealignFront + br * m * 16u + uint32_t(int32_t(sph) + start);
-                    const uint32_t q4 = q >> 2, sh = q & 3u;
-                    if (4u * (q4 + 5u) > lds.size()) return fail(RESHARD_EINVAL, "internal: staging read out of range");
-                    uint32_t wd[5];
-                    std::memcpy(wd, lds.data() + 4u * q4, sizeof(wd));
+                    const int32_t pos = int32_t(sph) + start;
+                    const int32_t j0 = pos >> 4;
+                    uint32_t w[8] = {0};
+                    if (j0 >= 0 && !load_word(o, sph, j0, w)) return fail(RESHARD_EINVAL, "internal: shifted load outside its row");
+                    if (16 * (j0 + 1) < int32_t(sph + run) && !load_word(o, sph, j0 + 1, w + 4))
+                        return fail(RESHARD_EINVAL, "internal: shifted load outside its row");
+                    const uint32_t sh = uint32_t(pos) & 15u, t4 = sh >> 2, b = sh & 3u;
                     uint32_t v[4];
-                    for (int t = 0; t < 4; ++t) v[t] = rs::align_byte(wd[t + 1], wd[t], sh);
+                    for (uint32_t t = 0; t < 4; ++t) v[t] = rs::align_byte(w[t4 + t + 1], w[t4 + t], b);
                     uint8_t bytes[16];
                     std::memcpy(bytes, v, 16);
                     for (uint32_t r = 0; r < d.nfan; ++r) {
                         char *dst = static_cast<char *>(dst_ptrs[p->fan[d.fan_off + r]]) + d.dst_base + o.dst;
-                        for (int32_t b = lo; b < hi; ++b) dst[b] = char(bytes[b - start]);
+                        for (int32_t c = lo; c < hi; ++c) dst[c] = char(bytes[c - start]);
                     }
                 }
+                continue;
             }
-            continue;
-        }
-        for (uint32_t v = d.v0; v < d.v1; ++v) {
-            const rs::Rel o = levels == 1   ? rs::chunk_offsets<1>(d, v, w)
-                              : levels == 2 ? rs::chunk_offsets<2>(d, v, w)
-                                            : rs::chunk_offsets<3>(d, v, w);
-            for (uint32_t r = 0; r < d.nfan; ++r) {
-                char *dst = static_cast<char *>(dst_ptrs[p->fan[d.fan_off + r]]) + d.dst_base;
-                std::memcpy(dst + o.dst, src + o.src, w);
+            if (rs::kind_realign(d.kind)) {
+                // Same staging layout, slot arithmetic and dword funnel shifts as
+                // the kernel's LDS path, with every staging access bounds-checked.
+                const uint32_t m = d.vpr, run = d.run, sb = uint32_t(d.src_base), db = uint32_t(d.dst_base);
+                lds.assign(rs::realign_lds_bytes(d.batch, m), 0);
+                auto row_off = [&](uint32_t row) {
+                    return levels == 1 ? rs::row_offsets<1>(d, row)
+                           : levels == 2 ? rs::row_offsets<2>(d, row) : rs::row_offsets<3>(d, row);
+                };
+                for (uint32_t r0 = d.v0; r0 < d.v1; r0 += d.batch) {
+                    const uint32_t nb = std::min(d.batch, d.v1 - r0);
+                    std::fill(lds.begin(), lds.end(), 0);
+                    for (uint32_t i = 0; i < nb * m; ++i) {
+                        const uint32_t br = rs::fastdiv(i, d.mul_vpr, d.sh_vpr), j = i - br * m;
+                        const rs::Rel o = row_off(r0 + br);
+                        const uint32_t ph = (sb + o.src) & 15u;
+                        if (16u * j >= ph + run) continue;
+                        const uint32_t at = rs::kRealignFront + 16u * i;
+                        if (at + 16u > lds.size()) return fail(RESHARD_EINVAL, "internal: staging write out of range");
+                        // the kernel's signed 32-bit word offset; copy only the
+                        // row's bytes of the aligned source word
+                        const int32_t off = int32_t(o.src + 16u * j - ph);
+                        const int64_t wbeg = int64_t(o.src) - ph + 16 * int64_t(j);
+                        if (int64_t(off) != wbeg) return fail(RESHARD_EINVAL, "internal: staging word offset wraps");
+                        if (((sb + uint32_t(off)) & 15u) != 0) return fail(RESHARD_EINVAL, "internal: staging word misaligned");
+                        for (int64_t b = 0; b < 16; ++b) {
+                            const int64_t pos = wbeg + b - int64_t(o.src);  // row-relative
+                            if (pos >= 0 && pos < int64_t(run)) lds[at + b] = uint8_t(src[wbeg + b]);
+                        }
+                    }
+                    for (uint32_t i = 0; i < nb * m; ++i) {
+                        const uint32_t br = rs::fastdiv(i, d.mul_vpr, d.sh_vpr), k = i - br * m;
+                        const rs::Rel o = row_off(r0 + br);
+                        const uint32_t sph = (sb + o.src) & 15u, tph = (db + o.dst) & 15u;
+                        const int32_t start = int32_t(16u * k) - int32_t(tph);
+                        const int32_t lo = std::max(start, 0), hi = std::min(start + 16, int32_t(run));
+                        if (lo >= hi) continue;
+                        const uint32_t q = rs::kRealignFront + br * m * 16u + uint32_t(int32_t(sph) + start);
+                        const uint32_t q4 = q >> 2, sh = q & 3u;
+                        if (4u * (q4 + 5u) > lds.size()) return fail(RESHARD_EINVAL, "internal: staging read out of range");
+                        uint32_t wd[5];
+                        std::memcpy(wd, lds.data() + 4u * q4, sizeof(wd));
+                        uint32_t v[4];
+                        for (int t = 0; t < 4; ++t) v[t] = rs::align_byte(wd[t + 1], wd[t], sh);
+                        uint8_t bytes[16];
+                        std::memcpy(bytes, v, 16);
+                        for (uint32_t r = 0; r < d.nfan; ++r) {
+                            char *dst = static_cast<char *>(dst_ptrs[p->fan[d.fan_off + r]]) + d.dst_base + o.dst;
+                            for (int32_t b = lo; b < hi; ++b) dst[b] = char(bytes[b - start]);
+                        }
+                    }
+                }
+                continue;
+            }
+            for (uint32_t v = d.v0; v < d.v1; ++v) {
+                const rs::Rel o = levels == 1   ? rs::chunk_offsets<1>(d, v, w)
+                                  : levels == 2 ? rs::chunk_offsets<2>(d, v, w)
+                                                : rs::chunk_offsets<3>(d, v, w);
+                for (uint32_t r = 0; r < d.nfan; ++r) {
+                    char *dst = static_cast<char *>(dst_ptrs[p->fan[d.fan_off + r]]) + d.dst_base;
+                    std::memcpy(dst + o.dst, src + o.src, w);
+                }
             }
         }
-    }
-    return RESHARD_OK;
+        return RESHARD_OK;
+    });
 }
 
 const char *reshard_last_error(void) { return rs::g_last_error.c_str(); }

@@ -29,10 +29,9 @@
 
 #include "../../include/reshard.h"
 #include "planner.hpp"
+#include "status.hpp"
 
 namespace rs {
-
-reshard_status_t fail(reshard_status_t st, const std::string &msg);
 
 #define RS_CONST __attribute__((address_space(4)))
 #define RS_GLOBAL __attribute__((address_space(1)))
@@ -959,51 +958,55 @@ void release_device_table(const Plan &p) {
 }  // namespace rs
 
 extern "C" reshard_status_t reshard_plan_upload(const reshard_plan_t *plan) {
-    using namespace rs;
-    const Plan *p = reinterpret_cast<const Plan *>(plan);
-    if (!p) return fail(RESHARD_EINVAL, "NULL plan");
-    if (p->descs.empty()) return RESHARD_OK;
-    int dev = -1;
-    const hipError_t e = hipGetDevice(&dev);
-    if (e != hipSuccess) return fail(RESHARD_EHIP, std::string("hipGetDevice: ") + hipGetErrorString(e));
-    const Desc *descs = nullptr;
-    const int32_t *fan = nullptr;
-    const Seg *segs = nullptr;
-    return device_table(*p, dev, &descs, &fan, &segs);
+    return rs::guarded([&]() -> reshard_status_t {
+        using namespace rs;
+        const Plan *p = reinterpret_cast<const Plan *>(plan);
+        if (!p) return fail(RESHARD_EINVAL, "NULL plan");
+        if (p->descs.empty()) return RESHARD_OK;
+        int dev = -1;
+        const hipError_t e = hipGetDevice(&dev);
+        if (e != hipSuccess) return fail(RESHARD_EHIP, std::string("hipGetDevice: ") + hipGetErrorString(e));
+        const Desc *descs = nullptr;
+        const int32_t *fan = nullptr;
+        const Seg *segs = nullptr;
+        return device_table(*p, dev, &descs, &fan, &segs);
+    });
 }
 
 extern "C" reshard_status_t reshard_execute(const reshard_plan_t *plan, void *const *src_ptrs,
                                             void *const *dst_ptrs, void *stream) {
-    using namespace rs;
-    const Plan *p = reinterpret_cast<const Plan *>(plan);
-    if (!p || !src_ptrs || !dst_ptrs) return fail(RESHARD_EINVAL, "NULL plan or pointer array");
-    for (int64_t k = 0; k < p->src.ndev; ++k) {
-        if (p->src_local_numel[k] == 0) continue;
-        if (!src_ptrs[k])
-            return fail(RESHARD_EINVAL, "source buffer " + std::to_string(k) + " is NULL but its shard is not empty");
-        if (reinterpret_cast<uintptr_t>(src_ptrs[k]) % uintptr_t(p->align))
-            return fail(RESHARD_EINVAL, "source buffer " + std::to_string(k) + " is not aligned to " +
-                                            std::to_string(p->align) + " bytes");
-    }
-    for (int64_t k = 0; k < p->dst.ndev; ++k) {
-        if (p->dst_local_numel[k] == 0) continue;
-        if (!dst_ptrs[k])
-            return fail(RESHARD_EINVAL,
-                        "destination buffer " + std::to_string(k) + " is NULL but its shard is not empty");
-        if (reinterpret_cast<uintptr_t>(dst_ptrs[k]) % uintptr_t(p->align))
-            return fail(RESHARD_EINVAL, "destination buffer " + std::to_string(k) + " is not aligned to " +
-                                            std::to_string(p->align) + " bytes");
-    }
-    if (p->descs.empty()) return RESHARD_OK;
-    int dev = -1;
-    hipError_t e = hipGetDevice(&dev);
-    if (e != hipSuccess) return fail(RESHARD_EHIP, std::string("hipGetDevice: ") + hipGetErrorString(e));
-    const Desc *descs = nullptr;
-    const int32_t *fan = nullptr;
-    const Seg *segs = nullptr;
-    reshard_status_t st = device_table(*p, dev, &descs, &fan, &segs);
-    if (st != RESHARD_OK) return st;
-    hipStream_t s = static_cast<hipStream_t>(stream);
-    if (p->src.ndev + p->dst.ndev <= 64) return launch<64>(*p, descs, fan, segs, src_ptrs, dst_ptrs, s);
-    return launch<RESHARD_MAX_BUFFERS>(*p, descs, fan, segs, src_ptrs, dst_ptrs, s);
+    return rs::guarded([&]() -> reshard_status_t {
+        using namespace rs;
+        const Plan *p = reinterpret_cast<const Plan *>(plan);
+        if (!p || !src_ptrs || !dst_ptrs) return fail(RESHARD_EINVAL, "NULL plan or pointer array");
+        for (int64_t k = 0; k < p->src.ndev; ++k) {
+            if (p->src_local_numel[k] == 0) continue;
+            if (!src_ptrs[k])
+                return fail(RESHARD_EINVAL, "source buffer " + std::to_string(k) + " is NULL but its shard is not empty");
+            if (reinterpret_cast<uintptr_t>(src_ptrs[k]) % uintptr_t(p->align))
+                return fail(RESHARD_EINVAL, "source buffer " + std::to_string(k) + " is not aligned to " +
+                                                std::to_string(p->align) + " bytes");
+        }
+        for (int64_t k = 0; k < p->dst.ndev; ++k) {
+            if (p->dst_local_numel[k] == 0) continue;
+            if (!dst_ptrs[k])
+                return fail(RESHARD_EINVAL,
+                            "destination buffer " + std::to_string(k) + " is NULL but its shard is not empty");
+            if (reinterpret_cast<uintptr_t>(dst_ptrs[k]) % uintptr_t(p->align))
+                return fail(RESHARD_EINVAL, "destination buffer " + std::to_string(k) + " is not aligned to " +
+                                                std::to_string(p->align) + " bytes");
+        }
+        if (p->descs.empty()) return RESHARD_OK;
+        int dev = -1;
+        hipError_t e = hipGetDevice(&dev);
+        if (e != hipSuccess) return fail(RESHARD_EHIP, std::string("hipGetDevice: ") + hipGetErrorString(e));
+        const Desc *descs = nullptr;
+        const int32_t *fan = nullptr;
+        const Seg *segs = nullptr;
+        reshard_status_t st = device_table(*p, dev, &descs, &fan, &segs);
+        if (st != RESHARD_OK) return st;
+        hipStream_t s = static_cast<hipStream_t>(stream);
+        if (p->src.ndev + p->dst.ndev <= 64) return launch<64>(*p, descs, fan, segs, src_ptrs, dst_ptrs, s);
+        return launch<RESHARD_MAX_BUFFERS>(*p, descs, fan, segs, src_ptrs, dst_ptrs, s);
+    });
 }

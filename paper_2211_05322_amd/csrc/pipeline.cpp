@@ -20,92 +20,91 @@
 #include <vector>
 
 #include "../../include/reshard.h"
-
-namespace rs {
-reshard_status_t fail(reshard_status_t st, const std::string &msg);
-}
+#include "status.hpp"
 
 extern "C" reshard_status_t reshard_pipeline_simulate(int32_t stages, int32_t microbatches, int32_t eager,
                                                       double t_fwd, double t_bwd, double t_comm_fwd,
                                                       double t_comm_bwd, int32_t serial_links,
                                                       double *latency_out, int32_t *peak_live_out) {
-    using rs::fail;
-    const int S = stages, M = microbatches;
-    if (S < 1 || M < 1 || S > 4096 || M > 1 << 20) return fail(RESHARD_EINVAL, "stages and micro-batches must be >= 1");
-    if (t_fwd < 0 || t_bwd < 0 || t_comm_fwd < 0 || t_comm_bwd < 0) return fail(RESHARD_EINVAL, "negative time");
-    // per-stage op lists: (is_backward, micro-batch)
-    std::vector<std::vector<std::pair<int, int>>> ops(S);
-    for (int s = 0; s < S; ++s) {
-        int w = eager ? 2 * (S - s) - 1 : S - s;
-        w = std::min(w, M);
-        int nf = 0, nb = 0;
-        for (; nf < w; ++nf) ops[s].push_back({0, nf});
-        while (nf < M) {
-            ops[s].push_back({1, nb++});
-            ops[s].push_back({0, nf++});
-        }
-        while (nb < M) ops[s].push_back({1, nb++});
-    }
-    const double NA = -1.0;
-    std::vector<std::vector<double>> f_done(S, std::vector<double>(M, NA)), b_done(S, std::vector<double>(M, NA));
-    std::vector<std::vector<double>> f_arrive(S, std::vector<double>(M, NA)), b_arrive(S, std::vector<double>(M, NA));
-    std::vector<double> link_fwd(S, 0.0), link_bwd(S, 0.0);  // link s: stage s -> s+1 / s+1 -> s
-    std::vector<size_t> pos(S, 0);
-    std::vector<double> stage_free(S, 0.0);
-    std::vector<int> live(S, 0), peak(S, 0);
-    size_t remaining = size_t(S) * size_t(M) * 2;
-    double latency = 0.0;
-    while (remaining) {
-        // run every stage whose next op is ready, earliest start first
-        int pick = -1;
-        double pick_t = 0.0;
+    return rs::guarded([&]() -> reshard_status_t {
+        using rs::fail;
+        const int S = stages, M = microbatches;
+        if (S < 1 || M < 1 || S > 4096 || M > 1 << 20) return fail(RESHARD_EINVAL, "stages and micro-batches must be >= 1");
+        if (t_fwd < 0 || t_bwd < 0 || t_comm_fwd < 0 || t_comm_bwd < 0) return fail(RESHARD_EINVAL, "negative time");
+        // per-stage op lists: (is_backward, micro-batch)
+        std::vector<std::vector<std::pair<int, int>>> ops(S);
         for (int s = 0; s < S; ++s) {
-            if (pos[s] == ops[s].size()) continue;
-            const auto op = ops[s][pos[s]];
-            double ready;
+            int w = eager ? 2 * (S - s) - 1 : S - s;
+            w = std::min(w, M);
+            int nf = 0, nb = 0;
+            for (; nf < w; ++nf) ops[s].push_back({0, nf});
+            while (nf < M) {
+                ops[s].push_back({1, nb++});
+                ops[s].push_back({0, nf++});
+            }
+            while (nb < M) ops[s].push_back({1, nb++});
+        }
+        const double NA = -1.0;
+        std::vector<std::vector<double>> f_done(S, std::vector<double>(M, NA)), b_done(S, std::vector<double>(M, NA));
+        std::vector<std::vector<double>> f_arrive(S, std::vector<double>(M, NA)), b_arrive(S, std::vector<double>(M, NA));
+        std::vector<double> link_fwd(S, 0.0), link_bwd(S, 0.0);  // link s: stage s -> s+1 / s+1 -> s
+        std::vector<size_t> pos(S, 0);
+        std::vector<double> stage_free(S, 0.0);
+        std::vector<int> live(S, 0), peak(S, 0);
+        size_t remaining = size_t(S) * size_t(M) * 2;
+        double latency = 0.0;
+        while (remaining) {
+            // run every stage whose next op is ready, earliest start first
+            int pick = -1;
+            double pick_t = 0.0;
+            for (int s = 0; s < S; ++s) {
+                if (pos[s] == ops[s].size()) continue;
+                const auto op = ops[s][pos[s]];
+                double ready;
+                if (op.first == 0) {
+                    ready = s == 0 ? 0.0 : f_arrive[s][op.second];
+                } else {
+                    ready = s == S - 1 ? f_done[s][op.second] : b_arrive[s][op.second];
+                }
+                if (ready < 0) continue;  // producer not done yet
+                const double t = std::max(stage_free[s], ready);
+                if (pick < 0 || t < pick_t) {
+                    pick = s;
+                    pick_t = t;
+                }
+            }
+            if (pick < 0) return fail(RESHARD_EINVAL, "internal: schedule deadlock");
+            const int s = pick;
+            const auto op = ops[s][pos[s]++];
+            const int m = op.second;
             if (op.first == 0) {
-                ready = s == 0 ? 0.0 : f_arrive[s][op.second];
+                const double fin = pick_t + t_fwd;
+                f_done[s][m] = fin;
+                stage_free[s] = fin;
+                peak[s] = std::max(peak[s], ++live[s]);
+                if (s + 1 < S) {
+                    const double st = serial_links ? std::max(fin, link_fwd[s]) : fin;
+                    f_arrive[s + 1][m] = st + t_comm_fwd;
+                    link_fwd[s] = st + t_comm_fwd;
+                }
+                latency = std::max(latency, fin);
             } else {
-                ready = s == S - 1 ? f_done[s][op.second] : b_arrive[s][op.second];
+                const double fin = pick_t + t_bwd;
+                b_done[s][m] = fin;
+                stage_free[s] = fin;
+                --live[s];
+                if (s > 0) {
+                    const double st = serial_links ? std::max(fin, link_bwd[s - 1]) : fin;
+                    b_arrive[s - 1][m] = st + t_comm_bwd;
+                    link_bwd[s - 1] = st + t_comm_bwd;
+                }
+                latency = std::max(latency, fin);
             }
-            if (ready < 0) continue;  // producer not done yet
-            const double t = std::max(stage_free[s], ready);
-            if (pick < 0 || t < pick_t) {
-                pick = s;
-                pick_t = t;
-            }
+            --remaining;
         }
-        if (pick < 0) return fail(RESHARD_EINVAL, "internal: schedule deadlock");
-        const int s = pick;
-        const auto op = ops[s][pos[s]++];
-        const int m = op.second;
-        if (op.first == 0) {
-            const double fin = pick_t + t_fwd;
-            f_done[s][m] = fin;
-            stage_free[s] = fin;
-            peak[s] = std::max(peak[s], ++live[s]);
-            if (s + 1 < S) {
-                const double st = serial_links ? std::max(fin, link_fwd[s]) : fin;
-                f_arrive[s + 1][m] = st + t_comm_fwd;
-                link_fwd[s] = st + t_comm_fwd;
-            }
-            latency = std::max(latency, fin);
-        } else {
-            const double fin = pick_t + t_bwd;
-            b_done[s][m] = fin;
-            stage_free[s] = fin;
-            --live[s];
-            if (s > 0) {
-                const double st = serial_links ? std::max(fin, link_bwd[s - 1]) : fin;
-                b_arrive[s - 1][m] = st + t_comm_bwd;
-                link_bwd[s - 1] = st + t_comm_bwd;
-            }
-            latency = std::max(latency, fin);
-        }
-        --remaining;
-    }
-    if (latency_out) *latency_out = latency;
-    if (peak_live_out)
-        for (int s = 0; s < S; ++s) peak_live_out[s] = peak[s];
-    return RESHARD_OK;
+        if (latency_out) *latency_out = latency;
+        if (peak_live_out)
+            for (int s = 0; s < S; ++s) peak_live_out[s] = peak[s];
+        return RESHARD_OK;
+    });
 }

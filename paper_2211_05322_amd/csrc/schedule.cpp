@@ -18,10 +18,9 @@
 
 #include "../../include/reshard.h"
 #include "planner.hpp"
+#include "status.hpp"
 
 namespace rs {
-
-reshard_status_t fail(reshard_status_t st, const std::string &msg);
 
 namespace {
 
@@ -277,56 +276,58 @@ extern "C" reshard_status_t reshard_schedule(const reshard_plan_t *plan, int64_t
                                              int64_t max_dfs_nodes, int64_t random_rounds, uint64_t seed,
                                              int64_t *sender_out, int64_t *start_out, int64_t *makespan_out,
                                              int64_t *lower_bound_out, int64_t *dfs_nodes_out) {
-    using namespace rs;
-    const Plan *p = reinterpret_cast<const Plan *>(plan);
-    if (!p) return fail(RESHARD_EINVAL, "NULL plan");
-    if (src_devices_per_host < 1 || dst_devices_per_host < 1)
-        return fail(RESHARD_EINVAL, "devices per host must be >= 1");
-    if (max_dfs_nodes < 0 || random_rounds < 0) return fail(RESHARD_EINVAL, "negative budget");
-    if (int(algo) < 0 || int(algo) > 4) return fail(RESHARD_EINVAL, "unknown scheduling algorithm");
-    const int hs = int((p->src.ndev + src_devices_per_host - 1) / src_devices_per_host);
-    const int hd = int((p->dst.ndev + dst_devices_per_host - 1) / dst_devices_per_host);
-    const int nhosts = hs + hd;
-    std::vector<STask> ts(p->tasks.size());
-    for (size_t i = 0; i < p->tasks.size(); ++i) {
-        const UnitTask &t = p->tasks[i];
-        ts[i].dur = t.bytes;
-        std::set<int32_t> c, r;
-        for (int64_t k = p->src.shard_devs_off[t.src_shard]; k < p->src.shard_devs_off[t.src_shard + 1]; ++k)
-            c.insert(int32_t(p->src.shard_devs[k] / src_devices_per_host));
-        for (int64_t k = p->dst.shard_devs_off[t.dst_shard]; k < p->dst.shard_devs_off[t.dst_shard + 1]; ++k)
-            r.insert(int32_t(hs + p->dst.shard_devs[k] / dst_devices_per_host));
-        ts[i].cand.assign(c.begin(), c.end());
-        ts[i].recv.assign(r.begin(), r.end());
-    }
-    Sched s;
-    int64_t nodes = 0;
-    switch (algo) {
-        case RESHARD_SCHED_NAIVE: s = naive(ts, nhosts); break;
-        case RESHARD_SCHED_LOAD_BALANCE: s = load_balance(ts, nhosts); break;
-        case RESHARD_SCHED_DFS: s = dfs(ts, nhosts, max_dfs_nodes, &nodes); break;
-        case RESHARD_SCHED_RANDOMIZED: s = randomized(ts, nhosts, random_rounds, seed); break;
-        case RESHARD_SCHED_ENSEMBLE: {
-            const Sched a = dfs(ts, nhosts, max_dfs_nodes, &nodes);
-            const Sched b = randomized(ts, nhosts, random_rounds, seed);
-            s = b.makespan < a.makespan ? b : a;
-            break;
+    return rs::guarded([&]() -> reshard_status_t {
+        using namespace rs;
+        const Plan *p = reinterpret_cast<const Plan *>(plan);
+        if (!p) return fail(RESHARD_EINVAL, "NULL plan");
+        if (src_devices_per_host < 1 || dst_devices_per_host < 1)
+            return fail(RESHARD_EINVAL, "devices per host must be >= 1");
+        if (max_dfs_nodes < 0 || random_rounds < 0) return fail(RESHARD_EINVAL, "negative budget");
+        if (int(algo) < 0 || int(algo) > 4) return fail(RESHARD_EINVAL, "unknown scheduling algorithm");
+        const int hs = int((p->src.ndev + src_devices_per_host - 1) / src_devices_per_host);
+        const int hd = int((p->dst.ndev + dst_devices_per_host - 1) / dst_devices_per_host);
+        const int nhosts = hs + hd;
+        std::vector<STask> ts(p->tasks.size());
+        for (size_t i = 0; i < p->tasks.size(); ++i) {
+            const UnitTask &t = p->tasks[i];
+            ts[i].dur = t.bytes;
+            std::set<int32_t> c, r;
+            for (int64_t k = p->src.shard_devs_off[t.src_shard]; k < p->src.shard_devs_off[t.src_shard + 1]; ++k)
+                c.insert(int32_t(p->src.shard_devs[k] / src_devices_per_host));
+            for (int64_t k = p->dst.shard_devs_off[t.dst_shard]; k < p->dst.shard_devs_off[t.dst_shard + 1]; ++k)
+                r.insert(int32_t(hs + p->dst.shard_devs[k] / dst_devices_per_host));
+            ts[i].cand.assign(c.begin(), c.end());
+            ts[i].recv.assign(r.begin(), r.end());
         }
-    }
-    for (size_t i = 0; i < p->tasks.size(); ++i) {
-        // the sender device: the task's lowest-indexed owner on the chosen host
-        const UnitTask &t = p->tasks[i];
-        int64_t dev = -1;
-        for (int64_t k = p->src.shard_devs_off[t.src_shard]; k < p->src.shard_devs_off[t.src_shard + 1]; ++k)
-            if (p->src.shard_devs[k] / src_devices_per_host == s.host[i]) {
-                dev = p->src.shard_devs[k];
+        Sched s;
+        int64_t nodes = 0;
+        switch (algo) {
+            case RESHARD_SCHED_NAIVE: s = naive(ts, nhosts); break;
+            case RESHARD_SCHED_LOAD_BALANCE: s = load_balance(ts, nhosts); break;
+            case RESHARD_SCHED_DFS: s = dfs(ts, nhosts, max_dfs_nodes, &nodes); break;
+            case RESHARD_SCHED_RANDOMIZED: s = randomized(ts, nhosts, random_rounds, seed); break;
+            case RESHARD_SCHED_ENSEMBLE: {
+                const Sched a = dfs(ts, nhosts, max_dfs_nodes, &nodes);
+                const Sched b = randomized(ts, nhosts, random_rounds, seed);
+                s = b.makespan < a.makespan ? b : a;
                 break;
             }
-        if (sender_out) sender_out[i] = dev;
-        if (start_out) start_out[i] = s.start[i];
-    }
-    if (makespan_out) *makespan_out = s.makespan;
-    if (lower_bound_out) *lower_bound_out = lower_bound(ts, nhosts);
-    if (dfs_nodes_out) *dfs_nodes_out = nodes;
-    return RESHARD_OK;
+        }
+        for (size_t i = 0; i < p->tasks.size(); ++i) {
+            // the sender device: the task's lowest-indexed owner on the chosen host
+            const UnitTask &t = p->tasks[i];
+            int64_t dev = -1;
+            for (int64_t k = p->src.shard_devs_off[t.src_shard]; k < p->src.shard_devs_off[t.src_shard + 1]; ++k)
+                if (p->src.shard_devs[k] / src_devices_per_host == s.host[i]) {
+                    dev = p->src.shard_devs[k];
+                    break;
+                }
+            if (sender_out) sender_out[i] = dev;
+            if (start_out) start_out[i] = s.start[i];
+        }
+        if (makespan_out) *makespan_out = s.makespan;
+        if (lower_bound_out) *lower_bound_out = lower_bound(ts, nhosts);
+        if (dfs_nodes_out) *dfs_nodes_out = nodes;
+        return RESHARD_OK;
+    });
 }
