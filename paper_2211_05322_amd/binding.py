@@ -125,16 +125,27 @@ def _dtype_code(dtype):
     return _DTYPES[name]
 
 
-def _ptrs(bufs):
-    out = (ctypes.c_void_p * max(1, len(bufs)))()
-    for i, b in enumerate(bufs):
-        if b is None:
-            out[i] = None
-        elif isinstance(b, int):
-            out[i] = b
-        else:
-            out[i] = b.data_ptr() if b.numel() > 0 else None
-    return out
+def _addr(b):
+    if b is None or isinstance(b, int):
+        return b
+    return b.data_ptr() if b.numel() > 0 else None
+
+
+def pointer_array(bufs):
+    """The `void *const *` array reshard_execute takes, built once.
+
+    `bufs` holds tensors (an empty one passes NULL), integer addresses or
+    None.  A caller that reshards the same buffers repeatedly can build the
+    two arrays once and pass them to every reshard_execute, which then skips
+    the per-buffer marshalling.  The array holds addresses only: the tensors
+    must stay alive (and unmoved) while it is in use.
+    """
+    if isinstance(bufs, ctypes.Array):
+        return bufs
+    return (ctypes.c_void_p * max(1, len(bufs)))(*[_addr(b) for b in bufs])
+
+
+_ptrs = pointer_array
 
 
 class Plan:
@@ -196,7 +207,11 @@ def reshard_plan_upload(plan):
 
 
 def reshard_execute(plan, src_bufs, dst_bufs, stream=None):
-    """Enqueue the reshard kernel on `stream` (default: torch's current stream)."""
+    """Enqueue the reshard kernel on `stream` (default: torch's current stream).
+
+    `src_bufs` / `dst_bufs`: one buffer per device (tensors, addresses or
+    None), or arrays from `pointer_array`.
+    """
     if len(src_bufs) != plan.n_src or len(dst_bufs) != plan.n_dst:
         raise ValueError(f"need {plan.n_src} source and {plan.n_dst} destination buffers")
     _check(load().reshard_execute(plan.handle, _ptrs(src_bufs), _ptrs(dst_bufs),

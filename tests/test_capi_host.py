@@ -437,3 +437,30 @@ def test_gather_used_by_column_split_workloads():
     for wid, w in WORKLOADS.items():
         p = plan_of(w.shape, w.dtype, w.src_mesh, w.src_spec, w.dst_mesh, w.dst_spec)
         assert (B.reshard_plan_gather_chunks(p) > 0) == (wid in (3, 5)), wid
+
+
+def test_pointer_array_marshalling():
+    """pointer_array: tensors (empty ones as NULL), addresses and None, built once and passed as is."""
+    import torch
+    full, empty = torch.zeros(8), torch.zeros(0)
+    arr = B.pointer_array([full, empty, None, 4096])
+    assert isinstance(arr, ctypes.Array) and len(arr) == 4
+    assert list(arr) == [full.data_ptr(), None, None, 4096]
+    assert B.pointer_array(arr) is arr
+    assert len(B.pointer_array([])) == 1  # never a zero-length array
+
+
+def test_prebuilt_pointer_arrays_drive_the_interpreter():
+    """The same plan run from lists and from pre-built arrays gives the oracle's bytes both times."""
+    import torch
+    shape, sm, ss, dm, ds = (8, 24, 40), (2, 2), "S^0 R S^1", (2, 2), "R S^{01} R"
+    x = torch.arange(int(np.prod(shape)), dtype=torch.int32).reshape(shape).numpy()
+    src = [torch.from_numpy(np.ascontiguousarray(a)) for a in oracle.shard(x, sm, ss)]
+    want = oracle.reshard([s.numpy() for s in src], shape, sm, ss, dm, ds)
+    p = B.reshard_plan(shape, "int32", sm, ss, dm, ds)
+    for prebuilt in (False, True):
+        dst = [torch.full(w.shape, -1, dtype=torch.int32) for w in want]
+        sp, dp = (B.pointer_array(src), B.pointer_array(dst)) if prebuilt else (src, dst)
+        B.load().reshard_debug_execute_host(p.handle, B._ptrs(sp), B._ptrs(dp))
+        for g, w in zip(dst, want):
+            assert np.array_equal(g.numpy(), w)
