@@ -59,6 +59,12 @@ def load(path=None):
     path = path or LIB_PATH
     if not os.path.exists(path):
         raise ImportError(f"libreshard.so not built at {path}; run `python -m paper_2211_05322_amd.build`")
+    # torch first: its HIP runtime (libamdhip64 from its own directory,
+    # soname libamdhip64.so.7) then satisfies the library's dependency on
+    # libamdhip64.so.7.  Opened the other way round, the process would map
+    # the system runtime for the library and torch's for its tensors and
+    # streams -- two HIP runtimes, with kernels registered in only one.
+    import torch  # noqa: F401
     lib = ctypes.CDLL(path)
     plan_args = [ctypes.c_int, _I64P, ctypes.c_int, ctypes.c_int, _I64P, ctypes.c_char_p,
                  ctypes.c_int, _I64P, ctypes.c_char_p, ctypes.c_uint]

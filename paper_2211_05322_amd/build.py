@@ -63,5 +63,27 @@ def build(verbose=False, extra_hip_flags=(), out=LIB):
     return out
 
 
+ROOT = os.path.dirname(PKG)
+C_CLIENT_SRC = os.path.join(ROOT, "tests", "c", "abi_gpu.c")
+C_CLIENT = os.path.join(ROOT, "tests", "c", "abi_gpu")
+ROOT_INCLUDE_HIP = os.path.join(ROCM, "include")
+
+
+def build_c_client(verbose=False):
+    """The C99 client of the C ABI that the GPU tests run (tests/c/abi_gpu.c):
+    gcc against include/reshard.h, the in-tree library and the HIP runtime,
+    no Python or torch in its process."""
+    if not os.path.exists(C_CLIENT_SRC):  # a tree without tests
+        return None
+    staged = C_CLIENT + ".tmp"
+    _run(["gcc", "-std=c99", "-O2", "-Wall", "-Wextra", "-Werror", "-pedantic", "-D__HIP_PLATFORM_AMD__",
+          "-I", os.path.join(ROOT, "include"), "-isystem", ROOT_INCLUDE_HIP, C_CLIENT_SRC,
+          "-L", PKG, "-lreshard", "-L", f"{ROCM}/lib", "-lamdhip64",
+          "-Wl,-rpath,$ORIGIN/../../paper_2211_05322_amd", f"-Wl,-rpath,{ROCM}/lib", "-o", staged], verbose)
+    os.replace(staged, C_CLIENT)
+    return C_CLIENT
+
+
 if __name__ == "__main__":
     print(build(verbose="-v" in sys.argv))
+    print(build_c_client(verbose="-v" in sys.argv))

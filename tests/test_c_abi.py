@@ -2,9 +2,11 @@
 alone links libreshard.so and runs host-only calls (plan, queries, the host
 interpreter, error paths).  CPU only."""
 
+import ast
 import os
 import shutil
 import subprocess
+import sys
 
 import pytest
 
@@ -24,3 +26,15 @@ def test_c99_client_against_header(tmp_path):
     assert r.returncode == 0, r.stderr
     r = subprocess.run([str(exe)], capture_output=True, text=True, timeout=120)
     assert r.returncode == 0 and r.stdout.strip() == "ok", r.stdout + r.stderr
+
+
+def test_binding_maps_one_hip_runtime():
+    """A script that loads the library through the binding before importing
+    torch itself still has exactly one HIP runtime mapped: the one torch's
+    tensors and streams come from."""
+    code = ("from paper_2211_05322_amd import binding as B; B.load(); import torch; "
+            "print(sorted({l.split()[-1] for l in open('/proc/self/maps') if 'libamdhip64' in l}))")
+    r = subprocess.run([sys.executable, "-c", code], capture_output=True, text=True, timeout=300, cwd=ROOT)
+    assert r.returncode == 0, r.stderr
+    maps = ast.literal_eval(r.stdout.strip().splitlines()[-1])
+    assert len(maps) == 1, maps
