@@ -574,6 +574,20 @@ __global__ __launch_bounds__(1024) void reshard_gather_kernel(KArgs<NPTR> args) 
 // 8 * kMaxSegs, segment starts (bytes within the row) at 20 * kMaxSegs.
 constexpr uint32_t kGatherULds = 24u * kMaxSegs;
 
+// Chunk order of the unaligned row gather: the dispatcher hands workgroups to
+// the 8 XCDs in turn, so blocks b, b + 8, ..., b + 8 (kUGroup - 1) share an
+// XCD and its L2; they take kUGroup consecutive chunks.  A sender row that
+// ends inside a cache line shares it with the sender's next row, which the
+// next chunk or the one after gathers: on one XCD that line is fetched once
+// (measured reads 1.09 x the unique bytes with round-robin chunks, 1.02 x in
+// runs of 16, same time), while the resident chunks still form one window
+// of the destination.  The grid is rounded up to whole runs of 8 kUGroup.
+constexpr uint32_t kUGroup = 16;
+
+__device__ __forceinline__ uint32_t grouped_chunk(uint32_t b) {
+    return (b / (8u * kUGroup)) * (8u * kUGroup) + (b & 7u) * kUGroup + (b >> 3) % kUGroup;
+}
+
 template <int NPTR>
 __device__ __forceinline__ void stage_segments_u(const Desc &d, const RS_CONST KArgs<NPTR> *a) {
     uint64_t *sp = reinterpret_cast<uint64_t *>(rs_lds);
@@ -754,7 +768,7 @@ template <int NPTR>
 __global__ __launch_bounds__(256) void reshard_gather_u_kernel(KArgs<NPTR> args) {
     const RS_CONST KArgs<NPTR> *a = (const RS_CONST KArgs<NPTR> *)__builtin_amdgcn_kernarg_segment_ptr();
     const uint32_t b = blockIdx.x;
-    const uint32_t idx = a->per_xcd ? (b & 7u) * a->per_xcd + (b >> 3) : b;
+    const uint32_t idx = a->per_xcd ? (b & 7u) * a->per_xcd + (b >> 3) : grouped_chunk(b);
     if (idx >= a->ndesc) return;
     const Desc d = load_desc(a, idx);
     stage_segments_u(d, a);
@@ -833,9 +847,9 @@ reshard_status_t device_table(const Plan &p, int dev, const Desc **descs, const 
 
 template <typename K, typename A>
 reshard_status_t launch_one(K kernel, A a, uint32_t ndesc, bool remap, uint32_t block, uint32_t lds,
-                            hipStream_t stream) {
+                            hipStream_t stream, uint32_t grid_multiple = 1) {
     a.ndesc = ndesc;
-    uint32_t grid = ndesc;
+    uint32_t grid = (ndesc + grid_multiple - 1u) / grid_multiple * grid_multiple;  // ndesc < 2^24
     a.per_xcd = 0;
     if (remap) {
         a.per_xcd = (ndesc + 7u) / 8u;
@@ -921,7 +935,7 @@ reshard_status_t launch(const Plan &p, const Desc *descs, const int32_t *fan, co
         a.descs = descs + n_direct + n_gather;
         const reshard_status_t st = launch_one(reshard_gather_u_kernel<NPTR>, a, n_gather_u, remap,
                                                block < 256u ? block : 256u,
-                                               ulds > kGatherULds ? ulds : kGatherULds, stream);
+                                               ulds > kGatherULds ? ulds : kGatherULds, stream, 8u * kUGroup);
         if (st != RESHARD_OK) return st;
     }
     if (n_realign) {
