@@ -105,7 +105,8 @@ typedef struct {
     int64_t chunk_bytes;    /* source bytes per workgroup chunk (default: 4..16 KiB, sized
                                so a large plan has >= 4096 chunks, larger past 64 GiB of
                                unique data); whole vectors */
-    int32_t block_threads;  /* threads per workgroup: 64, 128, 256, 512 or 1024 (default 256) */
+    int32_t block_threads;  /* threads per workgroup: 64, 128, 256, 512 or 1024; 0 = default:
+                               256, and 512 for direct chunks whose fan-out is 2 */
     int32_t max_wgs_per_cu; /* cap on resident workgroups per CU, 2..32, enforced by reserving
                                LDS per workgroup; 0 = default, chosen per kernel from its
                                fan-out (direct chunks: 16 waves per CU at fan-out <= 2, 12

@@ -104,7 +104,10 @@ reshard_status_t make_plan(int ndim, const int64_t *shape, reshard_dtype_t dtype
         if (cap != 0 && cap != -1 && (cap < 2 || cap > 32))
             return fail(RESHARD_EINVAL, "tuning.max_wgs_per_cu must be -1, 0 or 2..32");
         tn.chunk_bytes = tuning->chunk_bytes;
-        if (bt) tn.block_threads = bt;
+        if (bt) {
+            tn.block_threads = bt;
+            tn.block_is_default = false;
+        }
         tn.max_wgs_per_cu = cap;
         if (tuning->gather_band < 0) return fail(RESHARD_EINVAL, "tuning.gather_band is negative");
         tn.gather_band = tuning->gather_band;

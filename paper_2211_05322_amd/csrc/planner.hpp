@@ -45,6 +45,7 @@ struct UnitTask {
 struct Tuning {
     int64_t chunk_bytes = 0;   // 0: automatic
     int32_t block_threads = 256;
+    bool block_is_default = true;  // the caller left the block size to the library
     int32_t max_wgs_per_cu = 0;  // the caller's cap (0: none)
     bool cap_is_default = true;  // the caller left the cap to the library (chosen at launch)
     int32_t gather_band = 0;     // row gather: segments per column band (0: whole rows)
