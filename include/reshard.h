@@ -68,7 +68,8 @@ typedef enum {
                                       algorithm"); default is longest-first greedy
                                       balancing of sent bytes per device (Eq. 4). */
 #define RESHARD_XCD_REMAP 0x2u     /* give each of the 8 XCDs a contiguous run of the chunk
-                                      table (default: chunks start in table order). */
+                                      table (default: chunks start in table order, the
+                                      unaligned row gather's in runs of 16 per XCD). */
 #define RESHARD_TASK_ORDER 0x4u    /* keep the chunk table task by task (default: ordered by
                                       destination address -- receiver set, then offset -- so
                                       workgroups running together fill whole destination rows). */
