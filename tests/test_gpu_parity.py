@@ -336,6 +336,22 @@ def test_unaligned_gather_path(case):
         assert_same(got, want)
 
 
+@pytest.mark.parametrize("dm", [(1,), (2,)])
+@pytest.mark.parametrize("shape,n", [((2, 83, 390), 127), ((8, 21, 390), 128), ((13, 13, 390), 129),
+                                     ((2, 167, 390), 255), ((1, 337, 390), 257)])
+def test_unaligned_gather_chunk_counts_around_xcd_runs(shape, n, dm):
+    """The unaligned row gather hands chunks to the XCDs in runs of 16, on a
+    grid rounded up to whole rounds of 8 x 16 chunks: counts just below, at
+    and above such a round, with and without the XCD flag, one row group
+    gathered from 32 senders (26/24-byte segments)."""
+    args = (shape, "float16", (4, 8), "R R S^{01}", dm, "R R R")
+    _say(f"unaligned gather, {n} chunks: {shape} -> {dm}")
+    assert B.reshard_plan_unaligned_gather_chunks(B.reshard_plan(*args, chunk_bytes=1024)) == n
+    for flags in (0, B.RESHARD_XCD_REMAP):
+        got, want = run_gpu(*args, rand_bits(shape, "float16", n), flags=flags, chunk_bytes=1024)
+        assert_same(got, want)
+
+
 # ------------------------------------------------------------ maximum sizes
 
 def test_max_buffers_direct_and_gather():
