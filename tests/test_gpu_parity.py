@@ -380,6 +380,42 @@ def _check_against_boxes(x, dst, shape, mesh, spec):
         assert torch.equal(d.view(torch.int16), want.view(torch.int16)), f"destination {k} differs"
 
 
+def _table3():
+    import json
+    return json.load(open(os.path.join(os.path.dirname(os.path.abspath(__file__)), "golden", "table3_cases.json")))
+
+
+@pytest.mark.parametrize("case", range(1, 10))
+def test_table3_full_size_on_gpu(case):
+    """Table 3's nine cases at the tensor size Section 5.1.2 gives,
+    (1024, 1024, 512) (fp16, the element type the paper leaves open; 1 GiB),
+    with the readings of its garbled entries: each source shard is the tensor
+    sliced at the oracle's box, and every destination element is compared on
+    the GPU with the tensor sliced at the oracle's destination box."""
+    g = _table3()
+    c = g["cases"][case - 1]
+    shape = tuple(g["tensor_shape"])
+    sm, ss, dm, ds = tuple(c["send_mesh"]), c["send_spec"], tuple(c["recv_mesh"]), c["recv_spec"]
+    _say(f"table 3 case {case} at {shape}: {sm} {ss} -> {dm} {ds}")
+    x = make_workload_tensor(WORKLOADS[5].__class__("t3", shape, "float16", "bits", sm, ss, dm, ds),
+                             seed=case, device="cuda")
+    dims = oracle.parse_spec(ss, len(shape), len(sm))
+    src = []
+    for k in range(int(np.prod(sm))):
+        box = oracle.device_box(shape, sm, dims, k)
+        src.append(x[tuple(slice(lo, hi) for lo, hi in box)].contiguous())
+    p = B.reshard_plan(shape, "float16", sm, ss, dm, ds)
+    dst = B.empty_shards(p, 1)
+    for d in dst:
+        d.view(torch.int16).fill_(-1)
+    B.reshard_execute(p, src, dst)
+    torch.cuda.synchronize()
+    del src
+    _check_against_boxes(x, dst, shape, dm, ds)
+    del x, dst
+    torch.cuda.empty_cache()
+
+
 @pytest.mark.parametrize("case", [
     # one 5 GiB source to two 5 GiB replicas (offsets past 2^32 on both sides)
     ((5, 1 << 29), (1,), "RR", (2,), "RR"),
