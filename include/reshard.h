@@ -170,8 +170,10 @@ reshard_status_t reshard_plan_upload(const reshard_plan_t *plan);
  * destination devices) are device pointers on the current HIP device, each to
  * the dense C-order shard of that device, owned by the caller.  A pointer may
  * be NULL only if its shard is empty.  Pointers must be aligned to
- * reshard_plan_alignment() bytes.  Source and destination buffers must not
- * overlap.  `stream` is a hipStream_t (NULL = the null stream).
+ * reshard_plan_alignment() bytes.  A destination buffer must not overlap
+ * another destination buffer or any source buffer; source buffers may
+ * overlap one another (they are only read).  `stream` is a hipStream_t
+ * (NULL = the null stream).
  *
  * Asynchronous and stream-ordered: it enqueues one kernel per kind of chunk
  * the plan holds (one for every workload of the paper's shapes) and returns.
