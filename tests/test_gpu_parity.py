@@ -170,6 +170,22 @@ def test_launch_order_flags_and_residency_caps(flags, cap):
     assert_same(got, want)
 
 
+def test_replicated_sources_may_share_one_buffer():
+    """Sources are only read: the eight replicas of a replicated source may
+    all be the same device buffer (Table 3 case 2's specs, scaled)."""
+    shape, sm, ss, dm, ds = (64, 48, 40), (2, 4), "RRR", (2, 4), "S^0RR"
+    x = rand_bits(shape, "float16", 5)
+    xb = as_numpy_bits(x)
+    want = oracle.reshard([xb] * 8, shape, sm, ss, dm, ds)
+    p = B.reshard_plan(shape, "float16", sm, ss, dm, ds)
+    one = x.cuda()
+    dst = B.empty_shards(p, 1)
+    B.reshard_execute(p, [one] * 8, dst)
+    torch.cuda.synchronize()
+    assert torch.equal(one.cpu().view(torch.int16), x.view(torch.int16))
+    assert_same([d.cpu().numpy().view(np.uint16) for d in dst], want)
+
+
 def test_special_bit_patterns():
     bits = np.array([0x7E01, 0xFE02, 0x8000, 0x7C00, 0xFC00, 0x0001, 0x7FFF, 0xFFFF] * 64, dtype=np.uint16)
     x = torch.from_numpy(bits.view(np.float16).reshape(16, 32).copy())
