@@ -117,7 +117,7 @@ def main():
 
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
         print("bench.py measures one GPU only: every mesh device is a buffer on a single MI355X; "
-              "multi-GPU resharding is not part of this build (use --gpus 1)", file=sys.stderr)
+              "resharding across several GPUs is not implemented here (use --gpus 1)", file=sys.stderr)
         sys.exit(2)
 
     import torch
