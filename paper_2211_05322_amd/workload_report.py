@@ -73,7 +73,8 @@ def report_row(key, w, steps, flush_steps, scratch, stream):
     n_gather_u = B.reshard_plan_unaligned_gather_chunks(plan)
     n_direct = st["n_descriptors"] - n_gather - n_gather_u - n_realign
     dst = B.empty_shards(plan, 1)
-    run = lambda: B.reshard_execute(plan, src, dst, stream=stream)  # noqa: E731
+    sp0, dp0 = B.pointer_array(src), B.pointer_array(dst)  # built once, as a caller's loop would
+    run = lambda: B.reshard_execute(plan, sp0, dp0, stream=stream)  # noqa: E731
     for _ in range(5):
         run()
     torch.cuda.synchronize()
@@ -87,15 +88,13 @@ def report_row(key, w, steps, flush_steps, scratch, stream):
         s2 = B.empty_shards(scatter, 1)
         B.reshard_execute(scatter, [x], s2)
         sets.append((s2, B.empty_shards(plan, 1)))
-    ptrs = [(B._ptrs(s_), B._ptrs(d_)) for s_, d_ in sets]
-    lib = B.load()
-    h = plan.handle
+    ptrs = [(B.pointer_array(s_), B.pointer_array(d_)) for s_, d_ in sets]
     cur = [0]
 
     def run_rot():
         sp, dp = ptrs[cur[0] % nsets]
         cur[0] += 1
-        B._check(lib.reshard_execute(h, sp, dp, B.ctypes.c_void_p(stream.cuda_stream)))
+        B.reshard_execute(plan, sp, dp, stream=stream)
 
     for _ in range(nsets):
         run_rot()
