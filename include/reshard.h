@@ -83,7 +83,8 @@ typedef enum {
 #define RESHARD_NO_GATHER 0x100u   /* copy every unit task separately (default: tasks that share
                                       a receiver set and cut its rows into column segments --
                                       equal and 16-byte aligned, or of any width of at least 16
-                                      bytes over contiguous rows -- are written together, one
+                                      bytes over destination rows contiguous in runs of at least
+                                      one chunk -- are written together, one
                                       workgroup gathering destination rows or 16-byte slots
                                       from all their senders). */
 
@@ -111,7 +112,9 @@ typedef struct {
     int32_t max_wgs_per_cu; /* cap on resident workgroups per CU, 2..32, enforced by reserving
                                LDS per workgroup; 0 = default, chosen per kernel from its
                                fan-out (direct chunks: 16 waves per CU at fan-out <= 2, 12
-                               above; both row-gather kinds: 64 / fan-out waves, at least 8;
+                               above; both row-gather kinds: 64 / fan-out waves, at least 8,
+                               except unaligned row gathers with one sender per row, which
+                               take 32, 16, 12 and 8 waves at fan-out 1, 2, 3-4 and above;
                                never below 2 workgroups); -1 = no cap */
     int32_t gather_band;    /* row-gather chunks: column segments per band (>= 0); the chunks
                                of a row group cover one band of the destination rows after
@@ -231,11 +234,11 @@ int64_t reshard_plan_realign_chunks(const reshard_plan_t *plan);
  * (RESHARD_NO_GATHER turns them off), or -1 for a NULL plan. */
 int64_t reshard_plan_gather_chunks(const reshard_plan_t *plan);
 
-/* Number of workgroup chunks that write 16-byte slots of contiguous
- * destination rows gathered from several senders whose row segments have
- * any widths of at least 16 bytes and any byte alignment (uneven splits,
- * rows in different 16-byte phases; RESHARD_NO_GATHER turns them off), or
- * -1 for a NULL plan. */
+/* Number of workgroup chunks that write 16-byte slots of destination rows
+ * (contiguous, or contiguous in runs of at least one chunk) gathered from
+ * senders whose row segments have any widths of at least 16 bytes and any
+ * byte alignment (uneven splits, rows in different 16-byte phases;
+ * RESHARD_NO_GATHER turns them off), or -1 for a NULL plan. */
 int64_t reshard_plan_unaligned_gather_chunks(const reshard_plan_t *plan);
 
 /*

@@ -107,9 +107,11 @@ static_assert(sizeof(Desc) == 112, "descriptor layout is shared by host and devi
 //
 // Unaligned row gather (own section and kernel).  For row groups whose
 // segments tile the destination row in any widths of at least 16 bytes and
-// whose destination rows are contiguous, the chunks cover 16-byte slots of
-// the destination buffer itself (buffer-aligned, so a slot may hold the end
-// of one segment or row and the start of the next: at most two pieces).
+// whose destination rows are contiguous (or contiguous in runs, each run its
+// own region: its chunks carry its first row in row0), the chunks cover
+// 16-byte slots of the destination buffer itself (buffer-aligned, so a slot
+// may hold the end of one segment or row and the start of the next: at most
+// two pieces).
 // Fields: v1 = slots in the chunk (v0 = 0), dst_base = byte offset of its
 // first slot; vpr = row bytes with mul_vpr/sh_vpr; n1, n2 and their
 // multipliers = the source levels; ss[0] = row0 and ss[1] = cofs0 (int32):

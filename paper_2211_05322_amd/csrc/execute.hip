@@ -934,8 +934,16 @@ reshard_status_t launch(const Plan &p, const Desc *descs, const int32_t *fan, co
     if (n_gather_u) {
         uint32_t ulds = user_lds;
         if (p.tuning.cap_is_default) {
+            // Rows gathered from several senders: about 64 receiver write
+            // streams per CU, as the aligned gather.  One sender per row
+            // (rows in runs, or whole rows in another phase) reads like the
+            // direct kernel and wants its caps: measured uncapped best at
+            // fan-out 1, 16 waves at 2 (10 % faster than uncapped), 12 at 4
+            // (12 % faster than 16).
             const uint32_t fan = uint32_t(p.gather_u_fanout > 0 ? p.gather_u_fanout : 1);
-            ulds = residency_lds(64u / fan > 8u ? 64u / fan : 8u, block < 256u ? block : 256u);
+            uint32_t waves = 64u / fan > 8u ? 64u / fan : 8u;
+            if (p.gather_u_segs == 1) waves = fan <= 1 ? 32u : fan == 2 ? 16u : fan <= 4 ? 12u : 8u;
+            ulds = residency_lds(waves, block < 256u ? block : 256u);
         }
         a.descs = descs + n_direct + n_gather;
         const reshard_status_t st = launch_one(reshard_gather_u_kernel<NPTR>, a, n_gather_u, remap,

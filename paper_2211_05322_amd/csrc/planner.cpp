@@ -629,16 +629,25 @@ bool lower_gather_unaligned(Plan &p, const std::vector<size_t> &group, int64_t c
     if (at != dlo[nd - 1] + ext_d[nd - 1]) return false;
     const int64_t row_bytes = ext_d[nd - 1] * es;
     if (row_bytes >= (int64_t(1) << 31)) return false;
-    // destination rows contiguous: every outer extent but the outermost
-    // non-unit one spans its whole dimension
+    // destination rows: contiguous across the inner outer dimensions up to
+    // the first one that does not span its whole dimension; the dimensions
+    // from that one outward cut the group into runs of contiguous rows (one
+    // run when every inner extent is whole).  Row r of the group is its
+    // C-order index over the outer dimensions, so run k holds rows
+    // [k * run_rows, (k + 1) * run_rows).
     int64_t acc = row_bytes;
-    uint64_t rows = 1;
+    uint64_t rows = 1, run_rows = 1;
+    int brk = -1;
     for (int d = nd - 2; d >= 0; --d) {
         const int64_t n = t0.hi[d] - t0.lo[d];
-        if (n == 1) continue;
-        if (str_d[d] != acc) return false;
-        acc *= n;
         rows *= uint64_t(n);
+        if (n == 1 || brk >= 0) continue;
+        if (str_d[d] == acc) {
+            acc *= n;
+            run_rows *= uint64_t(n);
+        } else {
+            brk = d;
+        }
     }
     if (rows >= (uint64_t(1) << 31)) return false;
     // source levels: drop unit extents, merge dims contiguous on every sender
@@ -692,9 +701,10 @@ bool lower_gather_unaligned(Plan &p, const std::vector<size_t> &group, int64_t c
         // cache line within one workgroup.
         bool same_phase = row_bytes % 16 == 0 && (seg[0].src_base - d0) % 16 == 0;
         for (const auto &l : lv) same_phase = same_phase && l.ss[0] % 16 == 0;
+        for (int d = 0; d <= brk; ++d) same_phase = same_phase && str_d[d] % 16 == 0;
         if (same_phase) return false;
     }
-    const uint64_t total = rows * uint64_t(row_bytes);
+    const uint64_t run_bytes = run_rows * uint64_t(row_bytes);
     const int levels = std::max<int>(1, int(lv.size()));
     Desc d{};
     d.vpr = uint32_t(row_bytes);
@@ -714,37 +724,57 @@ bool lower_gather_unaligned(Plan &p, const std::vector<size_t> &group, int64_t c
     d.pad[0] = uint32_t(p.segs.size());
     d.pad[1] = uint32_t(ns);
     const uint64_t cv = uint64_t(std::max<int64_t>(16, chunk_bytes / 16)) / 16 * 16;
-    const uint64_t s_first = d0 / 16, s_end = (d0 + total + 15) / 16;
-    if (p.descs.size() + out.size() + (s_end - s_first + cv - 1) / cv > kMaxDescs) {
+    // runs shorter than a chunk stay with the per-task lowering: each run is
+    // chunked on its own, so short runs would make short chunks
+    if (brk >= 0 && (run_bytes < 16 * cv || rows / run_rows > kMaxDescs / 4)) return false;
+    // run starts in the receivers' buffers, C order over dimensions 0..brk
+    std::vector<uint64_t> run_d0(1, d0);
+    for (int d = 0; d <= brk; ++d) {
+        const int64_t n = t0.hi[d] - t0.lo[d];
+        std::vector<uint64_t> next;
+        next.reserve(run_d0.size() * uint64_t(n));
+        for (uint64_t b : run_d0)
+            for (int64_t i = 0; i < n; ++i) next.push_back(b + uint64_t(i * str_d[d]));
+        run_d0.swap(next);
+    }
+    uint64_t nchunks = 0;
+    for (uint64_t b : run_d0) nchunks += ((b + run_bytes + 15) / 16 - b / 16 + cv - 1) / cv;
+    if (p.descs.size() + out.size() + nchunks > kMaxDescs) {
         p.too_many = true;
         return false;
     }
     std::vector<Desc> mine;
-    for (uint64_t s0 = s_first; s0 < s_end; s0 += cv) {
-        const uint64_t nsl = std::min(cv, s_end - s0), base = 16 * s0;
-        d.v0 = 0;
-        d.v1 = uint32_t(nsl);
-        d.dst_base = base;
-        uint32_t row0 = 0;
-        int64_t cofs0;
-        if (base <= d0) {
-            cofs0 = int64_t(base) - int64_t(d0);  // in (-16, 0]
-        } else {
-            const uint64_t q = base - d0;
-            row0 = uint32_t(q / uint64_t(row_bytes));
-            cofs0 = int64_t(q - uint64_t(row0) * uint64_t(row_bytes));
+    mine.reserve(nchunks);
+    for (size_t k = 0; k < run_d0.size(); ++k) {
+        const uint64_t rd0 = run_d0[k];  // this run's first byte
+        const uint64_t s_first = rd0 / 16, s_end = (rd0 + run_bytes + 15) / 16;
+        for (uint64_t s0 = s_first; s0 < s_end; s0 += cv) {
+            const uint64_t nsl = std::min(cv, s_end - s0), base = 16 * s0;
+            d.v0 = 0;
+            d.v1 = uint32_t(nsl);
+            d.dst_base = base;
+            uint64_t row0 = uint64_t(k) * run_rows;
+            int64_t cofs0;
+            if (base <= rd0) {
+                cofs0 = int64_t(base) - int64_t(rd0);  // in (-16, 0]
+            } else {
+                const uint64_t q = base - rd0, dr = q / uint64_t(row_bytes);
+                row0 += dr;
+                cofs0 = int64_t(q - dr * uint64_t(row_bytes));
+            }
+            d.ss[0] = uint32_t(row0);
+            d.ss[1] = uint32_t(cofs0);
+            d.ss[2] = uint32_t(base < rd0 ? rd0 - base : 0);
+            d.src_rel0 = uint32_t(std::min<uint64_t>(16 * nsl, rd0 + run_bytes - base));
+            mine.push_back(d);
         }
-        d.ss[0] = row0;
-        d.ss[1] = uint32_t(cofs0);
-        d.ss[2] = uint32_t(base < d0 ? d0 - base : 0);
-        d.src_rel0 = uint32_t(std::min<uint64_t>(16 * nsl, d0 + total - base));
-        mine.push_back(d);
     }
     p.segs.insert(p.segs.end(), seg.begin(), seg.end());
     out.insert(out.end(), mine.begin(), mine.end());
     p.align = std::max<int64_t>(p.align, 16);
     p.max_fanout = std::max(p.max_fanout, nfan);
     p.gather_u_fanout = std::max(p.gather_u_fanout, nfan);
+    p.gather_u_segs = std::max(p.gather_u_segs, int64_t(ns));
     return true;
 }
 
@@ -768,6 +798,7 @@ void lower(Plan &p) {
     p.segs.clear();
     p.gather_fanout = 0;
     p.gather_u_fanout = 0;
+    p.gather_u_segs = 0;
     std::vector<Desc> gdescs, udescs;
     std::vector<char> handled(p.tasks.size(), 0);
     if (!(p.flags & 0x100u) && !(p.flags & 0x60u)) {

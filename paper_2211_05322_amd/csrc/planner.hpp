@@ -72,6 +72,7 @@ struct Plan {
     std::vector<Seg> segs;     // row-gather segment entries
     int64_t gather_fanout = 0; // largest receiver count among row-gather chunks
     int64_t gather_u_fanout = 0; // ... among unaligned row-gather chunks
+    int64_t gather_u_segs = 0;   // most segments per row among unaligned row-gather groups
     int64_t direct_fanout = 0; // largest receiver count among direct chunks
     size_t n_phase1 = 0;       // descs[0, n_phase1) run before descs[n_phase1, n_direct)
                                // (two launches; only the all-gather strategy has a second phase)

@@ -23,7 +23,8 @@ from paper_2211_05322_amd import build as _build
 
 pytestmark = pytest.mark.gpu
 
-# reshard_dtype_t codes of include/reshard.h
+# reshard_dtype_t codes of include/reshard.h; flags 0x100 = RESHARD_NO_GATHER,
+# 0x10 = RESHARD_LDS_STAGING
 _CODE = {"uint8": 0, "float16": 2, "float32": 4, "int64": 7}
 
 # (name, shape, dtype, src mesh, src spec, dst mesh, dst spec, block, stream, upload, repeat, flags)
@@ -37,8 +38,9 @@ CASES = [
      0, 0, 0, 1, 0),
     ("direct_block1024_uneven_h", (8, 64, 66, 64), "float16", (2, 2), "S^0 S^1 R R", (4, 2), "R R S^0 R",
      1024, 1, 0, 1, 0),
-    ("realign_shifted_loads_u8", (4, 130, 101), "uint8", (2,), "R S^0 R", (2,), "S^0 R R", 0, 0, 0, 1, 0),
-    ("realign_lds_staging_u8", (4, 130, 101), "uint8", (2,), "R S^0 R", (2,), "S^0 R R", 0, 1, 0, 1, 0x10),
+    ("realign_shifted_loads_u8", (4, 130, 101), "uint8", (2,), "R S^0 R", (2,), "S^0 R R", 0, 0, 0, 1, 0x100),
+    ("realign_lds_staging_u8", (4, 130, 101), "uint8", (2,), "R S^0 R", (2,), "S^0 R R", 0, 1, 0, 1, 0x110),
+    ("unaligned_gather_in_runs_u8", (4, 130, 101), "uint8", (2,), "R S^0 R", (2,), "S^0 R R", 0, 0, 0, 1, 0),
     ("empty_shards_int64", (3, 40), "int64", (4,), "S^0 R", (2, 2), "R S^1", 0, 0, 0, 1, 0),
     ("many_buffers_16x16_to_8x8", (32, 64), "float16", (16, 16), "S^0 S^1", (8, 8), "S^1 R", 0, 1, 1, 1, 0),
 ]

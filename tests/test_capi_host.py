@@ -226,6 +226,36 @@ def test_host_realign_path(case, chunk):
     host_case(shape, dt, sm, ss, dm, ds, flags=B.RESHARD_LDS_STAGING | ng, chunk_bytes=chunk)
 
 
+# Row groups whose destination rows are contiguous only in runs -- the
+# source split along a middle dimension, the destination along an outer one
+# -- with rows in different 16-byte phases: one unaligned-gather region per
+# run when every run holds at least a chunk, else the realignment path.
+RUN_CASES = [
+    ((4, 130, 101), "uint8", (2,), "R S^0 R", (2,), "S^0 R R"),
+    ((6, 130, 203), "uint8", (2,), "R S^0 R", (3,), "S^0 R R"),
+    ((4, 66, 130, 45), "uint8", (2, 2), "R S^0 S^1 R", (2,), "S^0 R R R"),   # runs over two levels
+    ((4, 41, 77), "float16", (2, 2), "R S^0 S^1", (2,), "S^0 R R"),          # two segments per row
+    ((10, 33, 150), "float32", (2,), "R S^0 R", (5, 2), "S^0 R R"),          # fan-out 2
+    ((4, 41, 77), "float16", (2, 2), "R S^0 S^1", (2, 3), "S^0 R R"),        # fan-out 3
+]
+
+
+@pytest.mark.parametrize("case", RUN_CASES)
+@pytest.mark.parametrize("chunk", [0, 256, 1024])
+def test_host_unaligned_gather_in_runs(case, chunk):
+    p = plan_of(*case, chunk_bytes=chunk)
+    if chunk:
+        assert B.reshard_plan_unaligned_gather_chunks(p) > 0 and B.reshard_plan_realign_chunks(p) == 0
+    host_case(*case, chunk_bytes=chunk)
+
+
+def test_short_runs_keep_the_realignment_path():
+    # runs of 21 or 20 rows x 154 bytes (about 3 KiB) are shorter than the
+    # automatic chunk of this small tensor (4 KiB)
+    p = plan_of((4, 41, 77), "float16", (2, 2), "R S^0 S^1", (2,), "S^0 R R")
+    assert B.reshard_plan_unaligned_gather_chunks(p) == 0 and B.reshard_plan_realign_chunks(p) > 0
+
+
 def test_aligned_workloads_do_not_realign():
     for w in WORKLOADS.values():
         p = plan_of(w.shape, w.dtype, w.src_mesh, w.src_spec, w.dst_mesh, w.dst_spec)

@@ -368,6 +368,33 @@ def test_unaligned_gather_chunk_counts_around_xcd_runs(shape, n, dm):
         assert_same(got, want)
 
 
+from tests.test_capi_host import RUN_CASES  # noqa: E402
+
+
+@pytest.mark.parametrize("case", RUN_CASES)
+def test_unaligned_gather_in_runs(case):
+    """Destination rows contiguous only in runs: one region per run."""
+    shape, dt, sm, ss, dm, ds = case
+    _say(f"unaligned gather in runs {case}")
+    for kw in ({}, {"chunk_bytes": 256}, {"chunk_bytes": 1024, "block_threads": 64}, {"chunk_bytes": 1024},
+               {"chunk_bytes": 1024, "flags": B.RESHARD_XCD_REMAP}):
+        got, want = run_gpu(shape, dt, sm, ss, dm, ds, rand_bits(shape, dt, 23), **kw)
+        assert_same(got, want)
+
+
+@pytest.mark.parametrize("dm", [(2,), (2, 2), (2, 4)])
+def test_unaligned_gather_in_runs_larger(dm):
+    """fp16 [4, 511, 1029]: 2058-byte rows, the middle dimension split 256/255
+    on the source and the outer one on the destination -- runs of 256 or 255
+    rows in different 16-byte phases, fan-out 1, 2 and 4."""
+    shape, sm, ss, ds = (4, 511, 1029), (2,), "R S^0 R", "S^0 R R"
+    _say(f"unaligned gather in runs {shape} -> {dm}")
+    p = B.reshard_plan(shape, "float16", sm, ss, dm, ds)
+    assert B.reshard_plan_unaligned_gather_chunks(p) > 0 and B.reshard_plan_realign_chunks(p) == 0
+    got, want = run_gpu(shape, "float16", sm, ss, dm, ds, rand_bits(shape, "float16", 29))
+    assert_same(got, want)
+
+
 # ------------------------------------------------------------ maximum sizes
 
 def test_max_buffers_direct_and_gather():
