@@ -102,6 +102,8 @@ def main():
                     help="broadcast (default) or a comparison strategy that re-reads slices per receiver")
     ap.add_argument("--seed", type=int, default=0)
     ap.add_argument("--chunk-bytes", type=int, default=0)
+    ap.add_argument("--max-wgs-per-cu", type=int, default=0,
+                    help="resident workgroups per CU (0: the library's choice per kernel; -1: no cap)")
     ap.add_argument("--block-threads", type=int, default=0)
     ap.add_argument("--flags", type=int, default=0)
     ap.add_argument("--buffer-sets", type=int, default=0,
@@ -148,7 +150,8 @@ def main():
 
     t0 = time.perf_counter()
     plan = B.reshard_plan(w.shape, w.dtype, w.src_mesh, w.src_spec, w.dst_mesh, w.dst_spec,
-                          flags=flags, chunk_bytes=args.chunk_bytes, block_threads=args.block_threads)
+                          flags=flags, chunk_bytes=args.chunk_bytes, block_threads=args.block_threads,
+                          max_wgs_per_cu=args.max_wgs_per_cu)
     plan_us = (time.perf_counter() - t0) * 1e6
     st = B.reshard_plan_stats(plan)
     dst = B.empty_shards(plan, 1)
@@ -228,7 +231,9 @@ def main():
             c.copy_(a)
         torch.cuda.synchronize()
         del a, c
-    traffic = measured_traffic(traffic_key(w.name, args.flags, args.strategy))
+    # the counter record holds the default tuning only
+    tuned = args.chunk_bytes or args.block_threads or args.max_wgs_per_cu
+    traffic = None if tuned else measured_traffic(traffic_key(w.name, args.flags, args.strategy))
     # The dominant kernel: the one that processes most of the plan's chunks
     # (an execute launches the direct, row-gather and realignment kernels for
     # the chunks of each kind the plan holds; most workloads use one).

@@ -110,12 +110,13 @@ typedef struct {
     int32_t block_threads;  /* threads per workgroup: 64, 128, 256, 512 or 1024; 0 = default:
                                256, and 512 for direct chunks whose fan-out is 2 */
     int32_t max_wgs_per_cu; /* cap on resident workgroups per CU, 2..32, enforced by reserving
-                               LDS per workgroup; 0 = default, chosen per kernel from its
-                               fan-out (direct chunks: 16 waves per CU at fan-out <= 2, 12
-                               above; both row-gather kinds: 64 / fan-out waves, at least 8,
-                               except unaligned row gathers with one sender per row, which
-                               take 32, 16, 12 and 8 waves at fan-out 1, 2, 3-4 and above;
-                               never below 2 workgroups); -1 = no cap */
+                               LDS per workgroup and rounded down to an even count (a CU's
+                               LDS is reserved in two halves); 0 = default, chosen per kernel
+                               from its fan-out (direct chunks: 16 waves per CU at fan-out
+                               <= 2, 8 above; both row-gather kinds: 64 / fan-out waves, at
+                               least 8, except unaligned row gathers with one sender per row,
+                               which take 32, 16 and 8 waves at fan-out 1, 2 and above; never
+                               below 2 workgroups); -1 = no cap */
     int32_t gather_band;    /* row-gather chunks: column segments per band (>= 0); the chunks
                                of a row group cover one band of the destination rows after
                                another; 0 = whole rows (default) */

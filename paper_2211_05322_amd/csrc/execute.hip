@@ -867,13 +867,20 @@ reshard_status_t launch_one(K kernel, A a, uint32_t ndesc, bool remap, uint32_t 
     return RESHARD_OK;
 }
 
-// LDS reservation (unused by the direct kernel; the gather kernel's segment
-// table fits inside it) that caps resident workgroups per CU at about
-// `waves` waves, never below 2 workgroups: the CU holds 160 KiB of LDS.
+// LDS reservation (unused by the direct kernel; the gather kernels' segment
+// tables fit inside it) that caps resident workgroups per CU.  The CU's
+// 160 KiB of LDS is handed out as two 80 KiB halves and a workgroup's
+// reservation must fit in one half (measured occupancy: reservations for 3
+// or 5 workgroups per CU leave 2 or 4 resident), so the cap is an even
+// number of workgroups: n per half.
+uint32_t lds_for_per_half(uint32_t n) {
+    if (n < 1u) n = 1u;
+    return n >= 16u ? 0u : (80u * 1024u / n) & ~1023u;
+}
+
+// ... for at most `waves` waves per CU, never below 2 workgroups.
 uint32_t residency_lds(uint32_t waves, uint32_t block) {
-    uint32_t wgs = waves / (block / 64u ? block / 64u : 1u);
-    if (wgs < 2u) wgs = 2u;
-    return wgs >= 32u ? 0u : (160u * 1024u / wgs) & ~1023u;
+    return lds_for_per_half(waves / (2u * (block / 64u ? block / 64u : 1u)));
 }
 
 template <int NPTR>
@@ -896,15 +903,15 @@ reshard_status_t launch(const Plan &p, const Desc *descs, const int32_t *fan, co
     // its stores, on half as many resident chunks (measured 1.5-4 % faster
     // on four fan-out-2 tensors, slower at fan-out 1, 4 and 8).
     const uint32_t dblock = p.tuning.block_is_default && p.direct_fanout == 2 ? 512u : block;
-    // Residency cap of the direct and gather kernels: the caller's, else
-    // chosen from the kernel's fan-out (measured with buffers that are not
-    // cache-resident): direct chunks 16 waves per CU at fan-out <= 2, 12
-    // above; gather chunks about 64 receiver write streams per CU (64 /
-    // fan-out waves, at least 8).
+    // Residency cap of the direct and gather kernels: the caller's (rounded
+    // down to an even number of workgroups), else chosen from the kernel's
+    // fan-out (measured with buffers that are not cache-resident): direct
+    // chunks 16 waves per CU at fan-out <= 2, 8 above; gather chunks about
+    // 64 receiver write streams per CU (64 / fan-out waves, at least 8).
     const uint32_t user_lds =
-        p.tuning.max_wgs_per_cu ? (160u * 1024u / uint32_t(p.tuning.max_wgs_per_cu)) & ~1023u : 0u;
+        p.tuning.max_wgs_per_cu ? lds_for_per_half(uint32_t(p.tuning.max_wgs_per_cu) / 2u) : 0u;
     const uint32_t cap_lds =
-        p.tuning.cap_is_default ? residency_lds(p.direct_fanout <= 2 ? 16u : 12u, dblock) : user_lds;
+        p.tuning.cap_is_default ? residency_lds(p.direct_fanout <= 2 ? 16u : 8u, dblock) : user_lds;
     const uint32_t n_direct = uint32_t(p.n_direct), n_gather = uint32_t(p.n_gather);
     const uint32_t n_gather_u = uint32_t(p.n_gather_u);
     const uint32_t n_realign = uint32_t(p.descs.size() - p.n_direct - p.n_gather - p.n_gather_u);
@@ -938,11 +945,11 @@ reshard_status_t launch(const Plan &p, const Desc *descs, const int32_t *fan, co
             // streams per CU, as the aligned gather.  One sender per row
             // (rows in runs, or whole rows in another phase) reads like the
             // direct kernel and wants its caps: measured uncapped best at
-            // fan-out 1, 16 waves at 2 (10 % faster than uncapped), 12 at 4
+            // fan-out 1, 16 waves at 2 (10 % faster than uncapped), 8 at 4
             // (12 % faster than 16).
             const uint32_t fan = uint32_t(p.gather_u_fanout > 0 ? p.gather_u_fanout : 1);
             uint32_t waves = 64u / fan > 8u ? 64u / fan : 8u;
-            if (p.gather_u_segs == 1) waves = fan <= 1 ? 32u : fan == 2 ? 16u : fan <= 4 ? 12u : 8u;
+            if (p.gather_u_segs == 1) waves = fan <= 1 ? 32u : fan == 2 ? 16u : 8u;
             ulds = residency_lds(waves, block < 256u ? block : 256u);
         }
         a.descs = descs + n_direct + n_gather;
