@@ -38,6 +38,8 @@ def main():
     ap = argparse.ArgumentParser(description=__doc__.splitlines()[0])
     ap.add_argument("--n", type=int, default=8192)
     ap.add_argument("--reps", type=int, default=20)
+    ap.add_argument("--max-wgs-per-cu", type=int, default=0,
+                    help="the reshard's residency cap (0: the library's; -1: none, so it reserves no LDS)")
     a = ap.parse_args()
     if not torch.cuda.is_available():
         raise SystemExit("no GPU visible")
@@ -49,7 +51,8 @@ def main():
     scatter = B.reshard_plan(w.shape, w.dtype, (1,), rep, w.src_mesh, w.src_spec, block_threads=1024)
     src = B.empty_shards(scatter, 1)
     B.reshard_execute(scatter, [x], src)
-    plan = B.reshard_plan(w.shape, w.dtype, w.src_mesh, w.src_spec, w.dst_mesh, w.dst_spec)
+    plan = B.reshard_plan(w.shape, w.dtype, w.src_mesh, w.src_spec, w.dst_mesh, w.dst_spec,
+                          max_wgs_per_cu=a.max_wgs_per_cu)
     dst = B.empty_shards(plan, 1)
     g = torch.Generator(device="cuda").manual_seed(0)
     A = torch.randn((a.n, a.n), generator=g, device="cuda", dtype=torch.float32).to(torch.bfloat16)
@@ -82,7 +85,9 @@ def main():
     flops = 2.0 * a.n ** 3
     st = B.reshard_plan_stats(plan)
     moved = st["bytes_read"] + st["bytes_written"]
-    print(f"{torch.cuda.get_device_name(0)}; {a.reps} repetitions; ms per repetition\n")
+    cap = {0: "the library's residency cap", -1: "no residency cap"}.get(a.max_wgs_per_cu,
+                                                                     f"{a.max_wgs_per_cu} workgroups per CU")
+    print(f"{torch.cuda.get_device_name(0)}; {a.reps} repetitions; reshard with {cap}; ms per repetition\n")
     print("| work | ms | rate |")
     print("|---|---|---|")
     print(f"| bf16 matmul {a.n}³ alone | {t_gemm:.3f} | {flops / t_gemm / 1e9:.0f} TFLOP/s |")
