@@ -603,7 +603,7 @@ def _fuzz_lowering(n, seed):
     return out
 
 
-@pytest.mark.parametrize("case", _fuzz_lowering(80, 2024))
+@pytest.mark.parametrize("case", _fuzz_lowering(400, 2024))
 def test_fuzz_lowering_flags_and_tunings(case):
     shape, dt, sm, ss, dm, ds, kw = case
     _say(f"lowering fuzz {case}")
