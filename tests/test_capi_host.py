@@ -168,6 +168,40 @@ def test_host_interpreter_fuzz(case):
     host_case(shape, dt, sm, ss, dm, ds, flags)
 
 
+def _fuzz_lowering(n, seed):
+    """Random tensors with longer rows (so every chunk kind occurs), random
+    meshes and specs, crossed with random lowering flags and tunings."""
+    rng = random.Random(seed)
+    flag_sets = [0, B.RESHARD_NO_GATHER, B.RESHARD_LDS_STAGING, B.RESHARD_NO_REALIGN | B.RESHARD_NO_GATHER,
+                 B.RESHARD_XCD_REMAP, B.RESHARD_TASK_ORDER | B.RESHARD_SENDER_NAIVE,
+                 B.RESHARD_STRATEGY_SENDRECV, B.RESHARD_STRATEGY_ALLGATHER]
+    out = []
+    while len(out) < n:
+        ndim = rng.randint(1, 4)
+        shape = tuple(rng.randint(1, 9) for _ in range(ndim - 1)) + (rng.randint(16, 700),)
+        sm = tuple(rng.randint(1, 4) for _ in range(rng.randint(1, 3)))
+        dm = tuple(rng.randint(1, 4) for _ in range(rng.randint(1, 3)))
+        kw = {"flags": rng.choice(flag_sets)}
+        if rng.random() < 0.7:
+            kw["chunk_bytes"] = rng.choice([64, 256, 1000, 4096, 20000])
+            kw["block_threads"] = rng.choice([64, 128, 256, 512, 1024])
+            kw["max_wgs_per_cu"] = rng.choice([0, -1, 2, 5])
+            kw["gather_band"] = rng.choice([0, 0, 1, 3])
+        out.append((shape, rng.choice(["uint8", "float16", "float32", "float64"]), sm,
+                    fmt_spec(random_dims(rng, ndim, len(sm))), dm, fmt_spec(random_dims(rng, ndim, len(dm))), kw))
+    return out
+
+
+@pytest.mark.parametrize("case", _fuzz_lowering(400, 2024))
+def test_host_lowering_fuzz(case):
+    """The GPU lowering fuzz's cases (every chunk kind, random flags and
+    tunings) through the host interpreter against the oracle."""
+    shape, dt, sm, ss, dm, ds, kw = case
+    kw = dict(kw)
+    flags = kw.pop("flags", 0)
+    host_case(shape, dt, sm, ss, dm, ds, flags, **kw)
+
+
 @pytest.mark.parametrize("chunk", [0, 16, 48, 1000, 4096])
 @pytest.mark.parametrize("case", _fuzz(12, 23, max_len=40))
 def test_host_interpreter_chunking(case, chunk):

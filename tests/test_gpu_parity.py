@@ -18,7 +18,7 @@ import oracle
 from paper_2211_05322_amd import binding as B
 from paper_2211_05322_amd.workloads import (UNEVEN_WORKLOADS, WORKLOADS, as_numpy_bits, make_workload_tensor,
                                             workload_by_name)
-from tests.test_capi_host import _fuzz
+from tests.test_capi_host import _fuzz, _fuzz_lowering
 from tests.test_oracle_pins import fmt_spec, random_dims
 
 pytestmark = pytest.mark.gpu
@@ -578,30 +578,6 @@ def test_concurrent_executes_share_one_plan():
 
 
 # ------------------------------------------- lowering flags x tunings fuzz
-
-def _fuzz_lowering(n, seed):
-    """Random tensors with longer rows (so every chunk kind occurs), random
-    meshes and specs, crossed with random lowering flags and tunings."""
-    rng = random.Random(seed)
-    flag_sets = [0, B.RESHARD_NO_GATHER, B.RESHARD_LDS_STAGING, B.RESHARD_NO_REALIGN | B.RESHARD_NO_GATHER,
-                 B.RESHARD_XCD_REMAP, B.RESHARD_TASK_ORDER | B.RESHARD_SENDER_NAIVE,
-                 B.RESHARD_STRATEGY_SENDRECV, B.RESHARD_STRATEGY_ALLGATHER]
-    out = []
-    while len(out) < n:
-        ndim = rng.randint(1, 4)
-        shape = tuple(rng.randint(1, 9) for _ in range(ndim - 1)) + (rng.randint(16, 700),)
-        sm = tuple(rng.randint(1, 4) for _ in range(rng.randint(1, 3)))
-        dm = tuple(rng.randint(1, 4) for _ in range(rng.randint(1, 3)))
-        kw = {"flags": rng.choice(flag_sets)}
-        if rng.random() < 0.7:
-            kw["chunk_bytes"] = rng.choice([64, 256, 1000, 4096, 20000])
-            kw["block_threads"] = rng.choice([64, 128, 256, 512, 1024])
-            kw["max_wgs_per_cu"] = rng.choice([0, -1, 2, 5])
-            kw["gather_band"] = rng.choice([0, 0, 1, 3])
-        out.append((shape, rng.choice(["uint8", "float16", "float32", "float64"]), sm,
-                    fmt_spec(random_dims(rng, ndim, len(sm))), dm, fmt_spec(random_dims(rng, ndim, len(dm))), kw))
-    return out
-
 
 @pytest.mark.parametrize("case", _fuzz_lowering(400, 2024))
 def test_fuzz_lowering_flags_and_tunings(case):
