@@ -23,3 +23,12 @@ def gpu_lib():
     from paper_2211_05322_amd import binding
 
     return binding.load()
+
+
+# A planted oracle mistake for tests/test_oracle_mutations.py, which runs the
+# pin tests in a child process with this variable set; never set otherwise.
+_MUTATION = os.environ.get("RESHARD_ORACLE_MUTATION")
+if _MUTATION:
+    from tests import oracle_mutations
+
+    oracle_mutations.apply(_MUTATION)
