@@ -14,6 +14,8 @@ import oracle
 # the module itself: the package re-exports the function `reshard` under the
 # submodule's name, so `import oracle.reshard as R` would bind that function
 R = importlib.import_module("oracle.reshard")
+SCH = importlib.import_module("oracle.schedule")
+PIPE = importlib.import_module("oracle.pipeline")
 
 
 def _split_ceil(length, k):
@@ -107,22 +109,94 @@ def _traffic_unique_writes(shape, itemsize, dst_mesh, dst_spec):
     return n * itemsize, n * itemsize
 
 
+# scheduling across hosts (Section 3.2)
+
+def _list_schedule_sender_only(model, order, host, nhosts):
+    # a task waits for its sender host only, not for its receivers
+    free = [0] * nhosts
+    start = [0] * len(model)
+    span = 0
+    for i in order:
+        dur, _, recv = model[i]
+        s = free[host[i]]
+        for h in [host[i]] + list(recv):
+            free[h] = s + dur
+        start[i] = s
+        span = max(span, s + dur)
+    return {"host": list(host), "start": start, "makespan": span}
+
+
+def _lower_bound_all_candidates(model, nhosts):
+    # every candidate sender charged as if it had to send
+    must = [0] * nhosts
+    lb = 0
+    for dur, cand, recv in model:
+        for h in list(recv) + list(cand):
+            must[h] += dur
+        lb = max(lb, dur)
+    return max([lb] + must)
+
+
+def _load_balance_shortest_first(model, nhosts):
+    order = sorted(range(len(model)), key=lambda i: (model[i][0], i))
+    load = [0] * nhosts
+    host = [None] * len(model)
+    for i in order:
+        best = min(model[i][1], key=lambda h: (load[h], h))
+        host[i] = best
+        load[best] += model[i][0]
+    return SCH.list_schedule(model, order, host, nhosts)
+
+
+# pipeline schedules (Section 4)
+
+def _stage_ops_warmup_plus_one(S, M, s, eager):
+    i = s + 1
+    w = 2 * (S - i) + 1 if eager else S - i + 2
+    w = min(w, M)
+    ops = [("F", m) for m in range(w)]
+    nf, nb = w, 0
+    while nf < M:
+        ops.append(("B", nb))
+        nb += 1
+        ops.append(("F", nf))
+        nf += 1
+    ops += [("B", m) for m in range(nb, M)]
+    return ops
+
+
+_STAGE_OPS = PIPE.stage_ops
+
+
+def _stage_ops_eager_ignored(S, M, s, eager):
+    return _STAGE_OPS(S, M, s, False)
+
+
+# name: (module, function, replacement, pin file, -k selection of its pins)
+_PINS_R = ("test_oracle_pins.py", None)
+_PINS_S = ("test_schedule.py", "not parity and not errors and not golden")
+_PINS_P = ("test_pipeline.py", "not parity and not errors")
 MUTATIONS = {
-    "split_ceil": ("split_bounds", _split_ceil),
-    "split_remainder_last": ("split_bounds", _split_remainder_last),
-    "shard_index_minor_major": ("shard_index", _shard_index_minor_major),
-    "device_coords_column_major": ("device_coords", _device_coords_column_major),
-    "lpt_shortest_first": ("choose_senders_lpt", _lpt_shortest_first),
-    "lpt_heaviest_sender": ("choose_senders_lpt", _lpt_heaviest_sender),
-    "naive_highest": ("choose_senders_naive", _naive_highest),
-    "unit_tasks_source_cuts_only": ("unit_tasks", _unit_tasks_source_cuts_only),
-    "unshard_without_replica_check": ("unshard", _unshard_without_replica_check),
-    "traffic_unique_writes": ("traffic_bytes", _traffic_unique_writes),
+    "split_ceil": (R, "split_bounds", _split_ceil, _PINS_R),
+    "split_remainder_last": (R, "split_bounds", _split_remainder_last, _PINS_R),
+    "shard_index_minor_major": (R, "shard_index", _shard_index_minor_major, _PINS_R),
+    "device_coords_column_major": (R, "device_coords", _device_coords_column_major, _PINS_R),
+    "lpt_shortest_first": (R, "choose_senders_lpt", _lpt_shortest_first, _PINS_R),
+    "lpt_heaviest_sender": (R, "choose_senders_lpt", _lpt_heaviest_sender, _PINS_R),
+    "naive_highest": (R, "choose_senders_naive", _naive_highest, _PINS_R),
+    "unit_tasks_source_cuts_only": (R, "unit_tasks", _unit_tasks_source_cuts_only, _PINS_R),
+    "unshard_without_replica_check": (R, "unshard", _unshard_without_replica_check, _PINS_R),
+    "traffic_unique_writes": (R, "traffic_bytes", _traffic_unique_writes, _PINS_R),
+    "schedule_sender_only": (SCH, "list_schedule", _list_schedule_sender_only, _PINS_S),
+    "lower_bound_all_candidates": (SCH, "lower_bound", _lower_bound_all_candidates, _PINS_S),
+    "load_balance_shortest_first": (SCH, "load_balance", _load_balance_shortest_first, _PINS_S),
+    "pipeline_warmup_plus_one": (PIPE, "stage_ops", _stage_ops_warmup_plus_one, _PINS_P),
+    "pipeline_eager_ignored": (PIPE, "stage_ops", _stage_ops_eager_ignored, _PINS_P),
 }
 
 
 def apply(name):
-    fn_name, fn = MUTATIONS[name]
-    setattr(R, fn_name, fn)
-    if hasattr(oracle, fn_name):
+    module, fn_name, fn, _ = MUTATIONS[name]
+    setattr(module, fn_name, fn)
+    if module is R and hasattr(oracle, fn_name):
         setattr(oracle, fn_name, fn)

@@ -1,9 +1,14 @@
-"""The oracle's pins catch plausible mistakes: each mutation in
-tests/oracle_mutations.py (a padding-style split, the remainder on the last
-shards, minor-major axis order, column-major devices, shortest-first or
-heaviest-sender balancing, the highest-index naive sender, destination cut
-points dropped, no replica check, replicas counted once in the traffic) is
-planted in a child process, and tests/test_oracle_pins.py must fail there.
+"""The oracles' pins catch plausible mistakes: each mutation in
+tests/oracle_mutations.py is planted in a child process, which runs the pin
+tests of that oracle (tests/test_oracle_pins.py, or the pin tests of
+tests/test_schedule.py and tests/test_pipeline.py -- not their parity tests
+against the library, which are no pins); they must fail there.  Resharding:
+a padding-style split, the remainder on the last shards, minor-major axis
+order, column-major devices, shortest-first or heaviest-sender balancing,
+the highest-index naive sender, destination cut points dropped, no replica
+check, replicas counted once in the traffic.  Scheduling: tasks that wait
+for their sender only, a lower bound charging every candidate, shortest-
+first balancing.  Pipeline: one warm-up forward too many, eagerness ignored.
 CPU only."""
 
 import os
@@ -15,15 +20,17 @@ import pytest
 from tests.oracle_mutations import MUTATIONS
 
 ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
-PINS = os.path.join(ROOT, "tests", "test_oracle_pins.py")
 
 
 def _run_pins(mutation):
-    env = dict(os.environ, RESHARD_ORACLE_MUTATION=mutation) if mutation else dict(os.environ)
+    pin_file, select = MUTATIONS[mutation][3]
+    env = dict(os.environ, RESHARD_ORACLE_MUTATION=mutation)
     env.pop("PYTEST_XDIST_WORKER", None)
-    return subprocess.run([sys.executable, "-m", "pytest", PINS, "-x", "-q", "-p", "no:cacheprovider",
-                           "-p", "no:randomly", "-m", "not gpu"],
-                          cwd=ROOT, env=env, capture_output=True, text=True, timeout=600)
+    cmd = [sys.executable, "-m", "pytest", os.path.join(ROOT, "tests", pin_file), "-x", "-q",
+           "-p", "no:cacheprovider", "-m", "not gpu"]
+    if select:
+        cmd += ["-k", select]
+    return subprocess.run(cmd, cwd=ROOT, env=env, capture_output=True, text=True, timeout=600)
 
 
 @pytest.mark.parametrize("mutation", sorted(MUTATIONS))

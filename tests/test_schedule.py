@@ -79,6 +79,16 @@ def test_lower_bound_is_tight_when_one_host_carries_everything():
     assert S.lower_bound(model, 3) == 12 == S.optimum(model, 3)
 
 
+def test_load_balance_visits_longest_first():
+    # Eq. 4 greedy, by hand: durations 1, 1, 2, each sendable from hosts 0
+    # or 1, each to its own receiver.  Longest first: the 2 goes to host 0,
+    # then both 1s to host 1 -> loads 2 and 2, makespan 2.  Shortest first
+    # would give host 0 a 1 and the 2 -> makespan 3.
+    model = [(1, [0, 1], [2]), (1, [0, 1], [3]), (2, [0, 1], [4])]
+    sched = S.load_balance(model, 5)
+    assert sched["host"] == [1, 1, 0] and sched["makespan"] == 2 and S.valid(model, sched)
+
+
 def test_randomized_depends_only_on_seed():
     rng = random.Random(3)
     model, nh = random_model(rng, 6, 3, 3)
