@@ -109,6 +109,19 @@ def _traffic_unique_writes(shape, itemsize, dst_mesh, dst_spec):
     return n * itemsize, n * itemsize
 
 
+_PARSE = R.parse_spec
+
+
+def _parse_spec_first_axis_only(spec, ndim, mesh_ndim):
+    # a multi-axis token such as S^{01} keeps only its first axis
+    return tuple(tuple(axes[:1]) for axes in _PARSE(spec, ndim, mesh_ndim))
+
+
+def _parse_spec_axes_reversed(spec, ndim, mesh_ndim):
+    # S^{01} read as S^{10}
+    return tuple(tuple(reversed(axes)) for axes in _PARSE(spec, ndim, mesh_ndim))
+
+
 # scheduling across hosts (Section 3.2)
 
 def _list_schedule_sender_only(model, order, host, nhosts):
@@ -187,6 +200,8 @@ MUTATIONS = {
     "unit_tasks_source_cuts_only": (R, "unit_tasks", _unit_tasks_source_cuts_only, _PINS_R),
     "unshard_without_replica_check": (R, "unshard", _unshard_without_replica_check, _PINS_R),
     "traffic_unique_writes": (R, "traffic_bytes", _traffic_unique_writes, _PINS_R),
+    "parse_spec_first_axis_only": (R, "parse_spec", _parse_spec_first_axis_only, _PINS_R),
+    "parse_spec_axes_reversed": (R, "parse_spec", _parse_spec_axes_reversed, _PINS_R),
     "schedule_sender_only": (SCH, "list_schedule", _list_schedule_sender_only, _PINS_S),
     "lower_bound_all_candidates": (SCH, "lower_bound", _lower_bound_all_candidates, _PINS_S),
     "load_balance_shortest_first": (SCH, "load_balance", _load_balance_shortest_first, _PINS_S),
