@@ -16,6 +16,7 @@ import oracle
 R = importlib.import_module("oracle.reshard")
 SCH = importlib.import_module("oracle.schedule")
 PIPE = importlib.import_module("oracle.pipeline")
+SCH._DFS = SCH.dfs  # the unmutated search, for the first-descent mutation
 
 
 def _split_ceil(length, k):
@@ -161,6 +162,16 @@ def _load_balance_shortest_first(model, nhosts):
     return SCH.list_schedule(model, order, host, nhosts)
 
 
+def _randomized_without_search(model, nhosts, rounds, seed):
+    # no random orders at all: the load-balance schedule
+    return SCH.load_balance(model, nhosts)
+
+
+def _dfs_first_descent(model, nhosts, max_nodes):
+    # the search stops at its first complete schedule
+    return SCH.__dict__["_DFS"](model, nhosts, 1)
+
+
 # pipeline schedules (Section 4)
 
 def _stage_ops_warmup_plus_one(S, M, s, eager):
@@ -205,6 +216,8 @@ MUTATIONS = {
     "schedule_sender_only": (SCH, "list_schedule", _list_schedule_sender_only, _PINS_S),
     "lower_bound_all_candidates": (SCH, "lower_bound", _lower_bound_all_candidates, _PINS_S),
     "load_balance_shortest_first": (SCH, "load_balance", _load_balance_shortest_first, _PINS_S),
+    "randomized_without_search": (SCH, "randomized", _randomized_without_search, _PINS_S),
+    "dfs_first_descent": (SCH, "dfs", _dfs_first_descent, _PINS_S),
     "pipeline_warmup_plus_one": (PIPE, "stage_ops", _stage_ops_warmup_plus_one, _PINS_P),
     "pipeline_eager_ignored": (PIPE, "stage_ops", _stage_ops_eager_ignored, _PINS_P),
 }

@@ -9,7 +9,8 @@ order, column-major devices, shortest-first or heaviest-sender balancing,
 the highest-index naive sender, destination cut points dropped, no replica
 check, replicas counted once in the traffic.  Scheduling: tasks that wait
 for their sender only, a lower bound charging every candidate, shortest-
-first balancing.  Pipeline: one warm-up forward too many, eagerness ignored.
+first balancing, the randomized search left out, DFS stopped at its first
+complete schedule.  Pipeline: one warm-up forward too many, eagerness ignored.
 CPU only."""
 
 import os
