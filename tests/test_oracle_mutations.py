@@ -13,6 +13,7 @@ first balancing, the randomized search left out, DFS stopped at its first
 complete schedule.  Pipeline: one warm-up forward too many, eagerness ignored.
 CPU only."""
 
+import concurrent.futures
 import os
 import subprocess
 import sys
@@ -35,8 +36,15 @@ def _run_pins(mutation):
     return subprocess.run(cmd, cwd=ROOT, env=env, capture_output=True, text=True, timeout=600)
 
 
+@pytest.fixture(scope="module")
+def outcomes():
+    """Every mutation's child run, four at a time."""
+    with concurrent.futures.ThreadPoolExecutor(max_workers=4) as pool:
+        return dict(zip(sorted(MUTATIONS), pool.map(_run_pins, sorted(MUTATIONS))))
+
+
 @pytest.mark.parametrize("mutation", sorted(MUTATIONS))
-def test_pins_catch_planted_mistake(mutation):
-    r = _run_pins(mutation)
+def test_pins_catch_planted_mistake(mutation, outcomes):
+    r = outcomes[mutation]
     # exit status 1: tests ran and at least one failed (2+ would be a broken run)
     assert r.returncode == 1, f"{mutation}: pins passed or the run broke ({r.returncode})\n{r.stdout[-3000:]}"
