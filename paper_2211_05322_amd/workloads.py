@@ -63,12 +63,22 @@ BENCH_WORKLOAD = 5
 
 # Workloads 5 and 3 with a last dimension that the shard count does not
 # divide: the balanced split gives segments of two widths whose rows sit in
-# different 16-byte phases on the two sides (the unaligned row-gather path).
+# different 16-byte phases on the two sides (the unaligned row-gather path);
+# and misaligned rows that reach their destination in runs.
 UNEVEN_WORKLOADS = {
     "uneven5": Workload("gpt3_act_fp16_8x2048x12300_hidden32_uneven_to_seq8x4rep", (8, 2048, 12300), "float16",
                         "normal", (4, 8), "R R S^{01}", (4, 8), "R S^1 R"),
     "uneven3": Workload("fp16_16x2048x5130_s01_uneven_to_replicated", (16, 2048, 5130), "float16", "normal",
                         (2, 4), "R R S^{01}", (2, 4), "R R R"),
+    # the middle dimension split 1024/1023 on the source and the outer one on
+    # the destination, with 24602-byte rows: destination rows contiguous only
+    # in runs of 1024 or 1023, in different 16-byte phases; fan-out 1, 2, 4
+    "runs1": Workload("fp16_8x2047x12301_mid_to_outer_runs_1rep", (8, 2047, 12301), "float16", "normal",
+                      (2,), "R S^0 R", (2,), "S^0 R R"),
+    "runs2": Workload("fp16_8x2047x12301_mid_to_outer_runs_2rep", (8, 2047, 12301), "float16", "normal",
+                      (2,), "R S^0 R", (2, 2), "S^0 R R"),
+    "runs4": Workload("fp16_8x2047x12301_mid_to_outer_runs_4rep", (8, 2047, 12301), "float16", "normal",
+                      (2,), "R S^0 R", (2, 4), "S^0 R R"),
 }
 
 
