@@ -3,10 +3,10 @@
     python -m paper_2211_05322_amd.workload_report [--steps 50] [--flush-steps 20] [--flush-mib 1024]
 
 For each workload (the five resharding tasks, workloads 5 and 3 with an
-uneven last dimension, then the one-sender replication microbenchmark at 1,
-4 and 8 receivers) prints one markdown row:
-unit tasks, fan-out, chunks per kernel, bytes moved (read + write), planning
-time, and three timings of `reshard_execute`:
+uneven last dimension, misaligned rows that arrive in runs, then the
+one-sender replication microbenchmark at 1, 4 and 8 receivers) prints one
+markdown row: unit tasks, fan-out, chunks per kernel, bytes moved (read +
+write), planning time, and four timings of `reshard_execute`:
 
 * back-to-back: mean of `--steps` consecutive launches on one set of
   buffers (HIP events on the launch stream around all of them), the way
@@ -17,7 +17,10 @@ time, and three timings of `reshard_execute`:
   the launches just before it;
 * cold: mean of `--flush-steps` launches, each preceded by a read-only pass
   over a `--flush-mib` scratch buffer (clean lines only, so the launch pays
-  no write-back of someone else's data), HIP events around each launch.
+  no write-back of someone else's data), HIP events around each launch;
+* graph: the back-to-back buffers, 50 executes captured into one HIP graph
+  (after `reshard_plan_upload`) and replayed, per reshard: what a caller
+  that replays its resharding saves on launch overhead.
 
 Each row ends with a round-trip check through the library (destination back
 to one buffer, compared bit for bit with the generated tensor).
@@ -44,6 +47,25 @@ def _time_back_to_back(fn, steps, stream):
     e1.record(stream)
     torch.cuda.synchronize()
     return e0.elapsed_time(e1) * 1e3 / steps
+
+
+def _time_graph(plan, sp, dp, per_graph=50, replays=10):
+    B.reshard_plan_upload(plan)  # the upload stays outside the capture
+    torch.cuda.synchronize()
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(g):
+        for _ in range(per_graph):
+            B.reshard_execute(plan, sp, dp)
+    g.replay()
+    torch.cuda.synchronize()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record()
+    for _ in range(replays):
+        g.replay()
+    e1.record()
+    torch.cuda.synchronize()
+    del g
+    return e0.elapsed_time(e1) * 1e3 / (per_graph * replays)
 
 
 def _time_cold(fn, steps, scratch, stream):
@@ -80,6 +102,7 @@ def report_row(key, w, steps, flush_steps, scratch, stream):
     torch.cuda.synchronize()
     warm_us = _time_back_to_back(run, steps, stream)
     cold_us = _time_cold(run, flush_steps, scratch, stream)
+    graph_us = _time_graph(plan, sp0, dp0)
     # rotated: distinct buffer sets in turn
     footprint = sum(t.numel() * t.element_size() for t in src + dst)
     nsets = min(64, max(2, -(-(4 << 30) // max(footprint, 1))))
@@ -113,7 +136,7 @@ def report_row(key, w, steps, flush_steps, scratch, stream):
            f"{plan_ms:.2f} | {warm_us:.1f} | {100 * gbs(warm_us) / HBM_PEAK_GBS:.1f} | "
            f"{rot_us:.1f} ({nsets}) | {100 * gbs(rot_us) / HBM_PEAK_GBS:.1f} | "
            f"{cold_us:.1f} | {100 * gbs(cold_us) / HBM_PEAK_GBS:.1f} | "
-           f"{'bit-exact' if ok else 'MISMATCH'} |")
+           f"{'bit-exact' if ok else 'MISMATCH'} | {graph_us:.1f} |")
     del x, src, dst, back
     torch.cuda.empty_cache()
     return row, ok
@@ -134,10 +157,11 @@ def main():
     scratch = torch.ones((a.flush_mib << 20) // 4, dtype=torch.int32, device="cuda")
     print(f"{torch.cuda.get_device_name(0)}; back-to-back: mean of {a.steps} launches; rotated: the same "
           f"over (n) buffer sets in turn; cold: mean of {a.flush_steps} launches, each after a read of "
-          f"{a.flush_mib} MiB; % of {HBM_PEAK_GBS:.0f} GB/s\n")
+          f"{a.flush_mib} MiB; graph: per reshard, 50 captured executes replayed; % of "
+          f"{HBM_PEAK_GBS:.0f} GB/s\n")
     print("| id | workload | unit tasks | fan-out | chunks direct/gather/unaligned gather/realign | MB moved | plan ms | "
-          "back-to-back µs | % | rotated µs (n) | % | cold µs | % | round trip |")
-    print("|---" * 14 + "|")
+          "back-to-back µs | % | rotated µs (n) | % | cold µs | % | round trip | graph µs |")
+    print("|---" * 15 + "|")
     all_ok = True
     for key in a.workloads.split(","):
         w = workload_by_name(key)
