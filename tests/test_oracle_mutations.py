@@ -1,15 +1,16 @@
 """The oracles' pins catch plausible mistakes: each mutation in
 tests/oracle_mutations.py is planted in a child process, which runs the pin
 tests of that oracle (tests/test_oracle_pins.py, or the pin tests of
-tests/test_schedule.py and tests/test_pipeline.py -- not their parity tests
-against the library, which are no pins); they must fail there.  Resharding:
+tests/test_schedule.py and tests/test_pipeline.py -- not their checks of
+the library, which are no pins); they must fail there.  Resharding:
 a multi-axis spec token kept to its first axis or read in reverse, a
 padding-style split, the remainder on the last shards, minor-major axis
 order, column-major devices, shortest-first or heaviest-sender balancing,
 the highest-index naive sender, destination cut points dropped, no replica
 check, replicas counted once in the traffic.  Scheduling: tasks that wait
-for their sender only, a lower bound charging every candidate, shortest-
-first balancing, the randomized search left out, DFS stopped at its first
+for their sender host only or for every earlier task, a lower bound
+charging every candidate, shortest-first balancing, the randomized search
+left out or cut to one random order per iteration, DFS stopped at its first
 complete schedule.  Pipeline: one warm-up forward too many, eagerness ignored.
 CPU only."""
 
