@@ -168,7 +168,11 @@ reshard_status_t reshard_plan_ex(int ndim, const int64_t *shape, reshard_dtype_t
 reshard_status_t reshard_plan_upload(const reshard_plan_t *plan);
 
 /*
- * Run the plan: fill every destination buffer from the source buffers.
+ * Run the plan: fill every destination buffer from the source buffers --
+ * the data movement of one cross-mesh resharding task (Section 2.2), each
+ * unit task moved as a broadcast from its chosen sender to all its
+ * receivers (Section 3.1), every unique slice read once (the lower bound of
+ * Section 2.2).
  *
  * src_ptrs[k] (k < number of source devices) and dst_ptrs[k] (k < number of
  * destination devices) are device pointers on the current HIP device, each to
@@ -177,7 +181,9 @@ reshard_status_t reshard_plan_upload(const reshard_plan_t *plan);
  * reshard_plan_alignment() bytes.  A destination buffer must not overlap
  * another destination buffer or any source buffer; source buffers may
  * overlap one another (they are only read).  `stream` is a hipStream_t
- * (NULL = the null stream).
+ * (NULL = the null stream), passed as void * so this header needs no HIP
+ * header and a plain C compiler can include it; hipStream_t is itself a
+ * pointer to an opaque struct, so the two are the same at the ABI.
  *
  * Asynchronous and stream-ordered: it enqueues one kernel per kind of chunk
  * the plan holds (one for every workload of the paper's shapes) and returns.
@@ -198,12 +204,17 @@ reshard_status_t reshard_plan_upload(const reshard_plan_t *plan);
 reshard_status_t reshard_execute(const reshard_plan_t *plan, void *const *src_ptrs,
                                  void *const *dst_ptrs, void *stream);
 
-/* Free a plan and its device table.  NULL is accepted.  The caller must make
- * sure no launched execute of this plan is still running. */
+/* Free a plan and its device table.  A plan is built once and reused
+ * because a resharding task repeats every training iteration (Section 2.2);
+ * this ends that reuse.  NULL is accepted.  The caller must make sure no
+ * launched execute of this plan is still running. */
 void reshard_plan_destroy(reshard_plan_t *plan);
 
 /* Shape of device `device`'s shard on side 0 (source) or 1 (destination):
- * writes ndim values to shape_out.  EINVAL for a bad side/device/NULL. */
+ * the extent of the data slice the device holds under its mesh and spec
+ * (Section 2.2, "Sharding spec"; the split of the appendix decomposition,
+ * balanced for lengths the shard count does not divide).  Writes ndim values
+ * to shape_out (caller-owned).  EINVAL for a bad side/device/NULL. */
 reshard_status_t reshard_plan_local_shape(const reshard_plan_t *plan, int side, int64_t device,
                                           int64_t *shape_out);
 
@@ -326,8 +337,10 @@ reshard_status_t reshard_pipeline_simulate(int32_t stages, int32_t microbatches,
                                            double t_comm_bwd, int32_t serial_links,
                                            double *latency_out, int32_t *peak_live_out);
 
-/* Text of the last error on the calling thread ("" if none).  Never NULL;
- * valid until the next call on the same thread. */
+/* Text of the last error on the calling thread ("" if none).  Not an
+ * operation of the paper: the error report of this interface, which never
+ * throws across it.  Never NULL; owned by the library; valid until the
+ * next call on the same thread. */
 const char *reshard_last_error(void);
 
 /* Library version string, e.g. "0.1.0". */
