@@ -33,6 +33,7 @@ sys.path.insert(0, ROOT)
 HBM_PEAK_GBS = 8000.0  # MI355X HBM3E, 8 TB/s
 METRIC = "effective resharding GB/s (read+write) and % of MI355X HBM peak, 1 GPU"
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "traffic_counters.json")
+SETUP_BLOCK = 128  # workgroup size of the setup and check launches (never the timed plan's default)
 KERNEL_SOURCES = [os.path.join(ROOT, "paper_2211_05322_amd", "csrc", f) for f in ("execute.hip", "desc.h", "planner.cpp")]
 
 
@@ -53,14 +54,19 @@ def traffic_key(workload_name, flags, strategy):
     return f"{workload_name}|flags={flags}|{strategy}"
 
 
-def measured_traffic(key):
-    """HBM bytes per launch from committed rocprofv3 counter runs, if they match this kernel."""
+def measured_traffic(key, bytes_read, bytes_written):
+    """HBM bytes per launch from committed rocprofv3 counter runs, if they
+    match this kernel.  A record whose reads or writes fall below the plan's
+    algorithmic bytes cannot be the timed launch's (every unique byte is read
+    and every replica written once), so it is not reported."""
     try:
         with open(TRAFFIC_FILE) as f:
             rec = json.load(f).get(key)
     except (OSError, ValueError):
         return None
     if not rec or rec.get("kernel_hash") != kernel_hash():
+        return None
+    if rec.get("fetch_bytes", 0) < bytes_read or rec.get("write_bytes", 0) < bytes_written:
         return None
     return rec.get("hbm_bytes_per_launch")
 
@@ -142,9 +148,10 @@ def main():
     # source mesh by the library itself (a reshard from one buffer).
     x = make_workload_tensor(w, seed=args.seed, device="cuda")
     rep = "".join("R" for _ in w.shape)
-    # (setup and check launches use 1024-thread workgroups so kernel traces
-    # tell them apart from the timed launches)
-    scatter = B.reshard_plan(w.shape, w.dtype, (1,), rep, w.src_mesh, w.src_spec, block_threads=1024)
+    # (setup and check launches use 128-thread workgroups, which every kernel
+    # honours, so kernel traces and counter runs tell them apart from the
+    # timed launches)
+    scatter = B.reshard_plan(w.shape, w.dtype, (1,), rep, w.src_mesh, w.src_spec, block_threads=SETUP_BLOCK)
     src = B.empty_shards(scatter, 1)
     B.reshard_execute(scatter, [x], src)
 
@@ -186,7 +193,7 @@ def main():
 
     # Round-trip check through the library: the dst of every set a step
     # wrote -> one buffer must equal x.
-    back_plan = B.reshard_plan(w.shape, w.dtype, w.dst_mesh, w.dst_spec, (1,), rep, block_threads=1024)
+    back_plan = B.reshard_plan(w.shape, w.dtype, w.dst_mesh, w.dst_spec, (1,), rep, block_threads=SETUP_BLOCK)
     back = B.empty_shards(back_plan, 1)
     roundtrip_ok = True
     for _, d_ in sets[:min(nsets, max(args.warmup, args.steps))]:
@@ -233,7 +240,8 @@ def main():
         del a, c
     # the counter record holds the default tuning only
     tuned = args.chunk_bytes or args.block_threads or args.max_wgs_per_cu
-    traffic = None if tuned else measured_traffic(traffic_key(w.name, args.flags, args.strategy))
+    traffic = None if tuned else measured_traffic(traffic_key(w.name, args.flags, args.strategy),
+                                                  st["bytes_read"], st["bytes_written"])
     # The dominant kernel: the one that processes most of the plan's chunks
     # (an execute launches the direct, row-gather and realignment kernels for
     # the chunks of each kind the plan holds; most workloads use one).
