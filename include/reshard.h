@@ -204,6 +204,30 @@ reshard_status_t reshard_plan_upload(const reshard_plan_t *plan);
 reshard_status_t reshard_execute(const reshard_plan_t *plan, void *const *src_ptrs,
                                  void *const *dst_ptrs, void *stream);
 
+/*
+ * As reshard_execute, for callers that cannot allocate device memory: code
+ * under HIP graph capture, tight serving loops, harnesses that forbid
+ * hipMalloc.  It allocates nothing: instead of a device table owned by the
+ * plan, it copies the plan's descriptor, receiver and segment tables
+ * (hipMemcpyAsync on `stream`) into a fixed scratch array that the library
+ * holds on every device it runs on, RESHARD_NOALLOC_MAX_TABLE_BYTES bytes,
+ * for the life of the process; the kernels are reshard_execute's.  Executing
+ * the same plan again on the same stream reuses the tables already there.
+ *
+ * Arguments, ownership and the buffers' layout are reshard_execute's.  All
+ * calls on one device share its scratch array, which keeps the last call's
+ * tables: calls that overlap on one device (another stream, another thread,
+ * a plan destroyed and another executed while kernels still run) race, and
+ * the caller must order them.  Nothing in the array needs clearing.
+ *
+ * Errors: those of reshard_execute, and EUNSUPPORTED when the plan's tables
+ * exceed RESHARD_NOALLOC_MAX_TABLE_BYTES (every workload of the paper's
+ * shapes needs at most 2.7 MiB; larger chunks shrink the table).
+ */
+#define RESHARD_NOALLOC_MAX_TABLE_BYTES (4u << 20)
+reshard_status_t reshard_execute_noalloc(const reshard_plan_t *plan, void *const *src_ptrs,
+                                         void *const *dst_ptrs, void *stream);
+
 /* Free a plan and its device table.  A plan is built once and reused
  * because a resharding task repeats every training iteration (Section 2.2);
  * this ends that reuse.  NULL is accepted.  The caller must make sure no

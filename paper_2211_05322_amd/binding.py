@@ -74,6 +74,8 @@ def load(path=None):
     lib.reshard_plan_ex.restype = ctypes.c_int
     lib.reshard_execute.argtypes = [ctypes.c_void_p, _VPP, _VPP, ctypes.c_void_p]
     lib.reshard_execute.restype = ctypes.c_int
+    lib.reshard_execute_noalloc.argtypes = [ctypes.c_void_p, _VPP, _VPP, ctypes.c_void_p]
+    lib.reshard_execute_noalloc.restype = ctypes.c_int
     lib.reshard_plan_destroy.argtypes = [ctypes.c_void_p]
     lib.reshard_plan_destroy.restype = None
     lib.reshard_plan_local_shape.argtypes = [ctypes.c_void_p, ctypes.c_int, ctypes.c_int64, _I64P]
@@ -222,6 +224,16 @@ def reshard_execute(plan, src_bufs, dst_bufs, stream=None):
         raise ValueError(f"need {plan.n_src} source and {plan.n_dst} destination buffers")
     _check(load().reshard_execute(plan.handle, _ptrs(src_bufs), _ptrs(dst_bufs),
                                   ctypes.c_void_p(_stream_handle(stream))))
+
+
+def reshard_execute_noalloc(plan, src_bufs, dst_bufs, stream=None):
+    """reshard_execute that allocates nothing: the plan's tables go to the
+    library's fixed per-device scratch array (see the header for its limit
+    and for calls that overlap)."""
+    if len(src_bufs) != plan.n_src or len(dst_bufs) != plan.n_dst:
+        raise ValueError(f"need {plan.n_src} source and {plan.n_dst} destination buffers")
+    _check(load().reshard_execute_noalloc(plan.handle, _ptrs(src_bufs), _ptrs(dst_bufs),
+                                          ctypes.c_void_p(_stream_handle(stream))))
 
 
 def reshard_debug_execute_host(plan, src_bufs, dst_bufs):

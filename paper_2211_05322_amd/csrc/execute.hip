@@ -1007,29 +1007,73 @@ extern "C" reshard_status_t reshard_plan_upload(const reshard_plan_t *plan) {
     });
 }
 
+namespace rs {
+namespace {
+
+// The caller's buffers: every non-empty shard has a pointer, aligned as the
+// plan's vectors need.
+reshard_status_t check_buffers(const Plan *p, void *const *src_ptrs, void *const *dst_ptrs) {
+    if (!p || !src_ptrs || !dst_ptrs) return fail(RESHARD_EINVAL, "NULL plan or pointer array");
+    for (int64_t k = 0; k < p->src.ndev; ++k) {
+        if (p->src_local_numel[k] == 0) continue;
+        if (!src_ptrs[k])
+            return fail(RESHARD_EINVAL, "source buffer " + std::to_string(k) + " is NULL but its shard is not empty");
+        if (reinterpret_cast<uintptr_t>(src_ptrs[k]) % uintptr_t(p->align))
+            return fail(RESHARD_EINVAL, "source buffer " + std::to_string(k) + " is not aligned to " +
+                                            std::to_string(p->align) + " bytes");
+    }
+    for (int64_t k = 0; k < p->dst.ndev; ++k) {
+        if (p->dst_local_numel[k] == 0) continue;
+        if (!dst_ptrs[k])
+            return fail(RESHARD_EINVAL,
+                        "destination buffer " + std::to_string(k) + " is NULL but its shard is not empty");
+        if (reinterpret_cast<uintptr_t>(dst_ptrs[k]) % uintptr_t(p->align))
+            return fail(RESHARD_EINVAL, "destination buffer " + std::to_string(k) + " is not aligned to " +
+                                            std::to_string(p->align) + " bytes");
+    }
+    return RESHARD_OK;
+}
+
+reshard_status_t launch_any(const Plan &p, const Desc *descs, const int32_t *fan, const Seg *segs,
+                            void *const *src_ptrs, void *const *dst_ptrs, hipStream_t s) {
+    if (p.src.ndev + p.dst.ndev <= 64) return launch<64>(p, descs, fan, segs, src_ptrs, dst_ptrs, s);
+    return launch<RESHARD_MAX_BUFFERS>(p, descs, fan, segs, src_ptrs, dst_ptrs, s);
+}
+
+}  // namespace
+
+// Scratch of reshard_execute_noalloc: the plan's descriptor, receiver and
+// segment tables are copied here (same layout as the plan's own device
+// table) instead of into memory the library allocates.  Each device holds
+// one copy for the life of the process.  Host code never passes the array's
+// name to a kernel or a copy: it passes the device address that
+// hipGetSymbolAddress returned on that device.
+static __device__ __align__(256) unsigned char scratch[RESHARD_NOALLOC_MAX_TABLE_BYTES];
+
+namespace {
+
+struct ScratchState {
+    std::mutex mu;
+    void *addr[Plan::kMaxHipDevices] = {};           // device address of `scratch`, per device
+    uint64_t plan[Plan::kMaxHipDevices] = {};        // serial of the plan whose tables it holds
+    void *stream[Plan::kMaxHipDevices] = {};         // the stream that copy was ordered on
+};
+
+ScratchState &scratch_state() {
+    static ScratchState st;
+    return st;
+}
+
+}  // namespace
+}  // namespace rs
+
 extern "C" reshard_status_t reshard_execute(const reshard_plan_t *plan, void *const *src_ptrs,
                                             void *const *dst_ptrs, void *stream) {
     return rs::guarded([&]() -> reshard_status_t {
         using namespace rs;
         const Plan *p = reinterpret_cast<const Plan *>(plan);
-        if (!p || !src_ptrs || !dst_ptrs) return fail(RESHARD_EINVAL, "NULL plan or pointer array");
-        for (int64_t k = 0; k < p->src.ndev; ++k) {
-            if (p->src_local_numel[k] == 0) continue;
-            if (!src_ptrs[k])
-                return fail(RESHARD_EINVAL, "source buffer " + std::to_string(k) + " is NULL but its shard is not empty");
-            if (reinterpret_cast<uintptr_t>(src_ptrs[k]) % uintptr_t(p->align))
-                return fail(RESHARD_EINVAL, "source buffer " + std::to_string(k) + " is not aligned to " +
-                                                std::to_string(p->align) + " bytes");
-        }
-        for (int64_t k = 0; k < p->dst.ndev; ++k) {
-            if (p->dst_local_numel[k] == 0) continue;
-            if (!dst_ptrs[k])
-                return fail(RESHARD_EINVAL,
-                            "destination buffer " + std::to_string(k) + " is NULL but its shard is not empty");
-            if (reinterpret_cast<uintptr_t>(dst_ptrs[k]) % uintptr_t(p->align))
-                return fail(RESHARD_EINVAL, "destination buffer " + std::to_string(k) + " is not aligned to " +
-                                                std::to_string(p->align) + " bytes");
-        }
+        reshard_status_t st = check_buffers(p, src_ptrs, dst_ptrs);
+        if (st != RESHARD_OK) return st;
         if (p->descs.empty()) return RESHARD_OK;
         int dev = -1;
         hipError_t e = hipGetDevice(&dev);
@@ -1037,10 +1081,71 @@ extern "C" reshard_status_t reshard_execute(const reshard_plan_t *plan, void *co
         const Desc *descs = nullptr;
         const int32_t *fan = nullptr;
         const Seg *segs = nullptr;
-        reshard_status_t st = device_table(*p, dev, &descs, &fan, &segs);
+        st = device_table(*p, dev, &descs, &fan, &segs);
         if (st != RESHARD_OK) return st;
+        return launch_any(*p, descs, fan, segs, src_ptrs, dst_ptrs, static_cast<hipStream_t>(stream));
+    });
+}
+
+extern "C" reshard_status_t reshard_execute_noalloc(const reshard_plan_t *plan, void *const *src_ptrs,
+                                                    void *const *dst_ptrs, void *stream) {
+    return rs::guarded([&]() -> reshard_status_t {
+        using namespace rs;
+        const Plan *p = reinterpret_cast<const Plan *>(plan);
+        reshard_status_t st = check_buffers(p, src_ptrs, dst_ptrs);
+        if (st != RESHARD_OK) return st;
+        if (p->descs.empty()) return RESHARD_OK;
+        const size_t dbytes = p->descs.size() * sizeof(Desc);
+        const size_t fbytes = p->fan.size() * sizeof(int32_t);
+        const size_t soff = (dbytes + fbytes + 15) & ~size_t(15);
+        const size_t total = soff + p->segs.size() * sizeof(Seg);
+        if (total > size_t(RESHARD_NOALLOC_MAX_TABLE_BYTES))
+            return fail(RESHARD_EUNSUPPORTED, "the plan's tables take " + std::to_string(total) +
+                                                  " bytes; reshard_execute_noalloc holds at most " +
+                                                  std::to_string(RESHARD_NOALLOC_MAX_TABLE_BYTES) +
+                                                  " (use reshard_execute, or larger chunks)");
+        int dev = -1;
+        hipError_t e = hipGetDevice(&dev);
+        if (e != hipSuccess) return fail(RESHARD_EHIP, std::string("hipGetDevice: ") + hipGetErrorString(e));
+        if (dev < 0 || dev >= Plan::kMaxHipDevices)
+            return fail(RESHARD_EUNSUPPORTED, "HIP device ordinal " + std::to_string(dev) + " above the limit");
         hipStream_t s = static_cast<hipStream_t>(stream);
-        if (p->src.ndev + p->dst.ndev <= 64) return launch<64>(*p, descs, fan, segs, src_ptrs, dst_ptrs, s);
-        return launch<RESHARD_MAX_BUFFERS>(*p, descs, fan, segs, src_ptrs, dst_ptrs, s);
+        char *base = nullptr;
+        {
+            ScratchState &ss = scratch_state();
+            std::lock_guard<std::mutex> lock(ss.mu);
+            if (!ss.addr[dev]) {
+                void *addr = nullptr;
+                e = hipGetSymbolAddress(&addr, HIP_SYMBOL(scratch));
+                if (e != hipSuccess || !addr) {
+                    (void)hipGetLastError();
+                    return fail(RESHARD_EHIP, std::string("hipGetSymbolAddress of the scratch table: ") +
+                                                  hipGetErrorString(e));
+                }
+                ss.addr[dev] = addr;
+            }
+            base = static_cast<char *>(ss.addr[dev]);
+            // The tables are copied on the call's stream, so its kernels see
+            // them; the same plan executed again on the same stream finds
+            // them in place.  Nothing in the scratch must start at zero: the
+            // kernels only read what the copy wrote.
+            if (ss.plan[dev] != p->serial || ss.stream[dev] != stream) {
+                ss.plan[dev] = 0;
+                e = hipMemcpyAsync(base, p->descs.data(), dbytes, hipMemcpyHostToDevice, s);
+                if (e == hipSuccess && fbytes)
+                    e = hipMemcpyAsync(base + dbytes, p->fan.data(), fbytes, hipMemcpyHostToDevice, s);
+                if (e == hipSuccess && !p->segs.empty())
+                    e = hipMemcpyAsync(base + soff, p->segs.data(), total - soff, hipMemcpyHostToDevice, s);
+                if (e != hipSuccess) {
+                    (void)hipGetLastError();
+                    return fail(RESHARD_EHIP, std::string("copy of the plan's tables into the scratch: ") +
+                                                  hipGetErrorString(e));
+                }
+                ss.plan[dev] = p->serial;
+                ss.stream[dev] = stream;
+            }
+        }
+        return launch_any(*p, reinterpret_cast<const Desc *>(base), reinterpret_cast<const int32_t *>(base + dbytes),
+                          reinterpret_cast<const Seg *>(base + soff), src_ptrs, dst_ptrs, s);
     });
 }

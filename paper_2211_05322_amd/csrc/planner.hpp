@@ -14,6 +14,7 @@
 //              (descriptors, one per workgroup)
 #pragma once
 
+#include <atomic>
 #include <cstdint>
 #include <mutex>
 #include <string>
@@ -51,7 +52,15 @@ struct Tuning {
     int32_t gather_band = 0;     // row gather: segments per column band (0: whole rows)
 };
 
+// A number no other plan of this process has (plans are told apart by it,
+// not by address, which a later plan may reuse).
+inline uint64_t next_plan_serial() {
+    static std::atomic<uint64_t> n{0};
+    return ++n;
+}
+
 struct Plan {
+    const uint64_t serial = next_plan_serial();
     int ndim = 0;
     std::vector<int64_t> shape;
     int64_t es = 0;            // element size in bytes
