@@ -24,7 +24,11 @@ Readings of the paper used below (the paper is silent or garbled there):
   j*floor(l/k) + min(j, l mod k), so the first (l mod k) shards are one
   element longer (66 into 4 gives 17,17,16,16).  For even lengths this is
   the appendix's "k equal size" cut at l/k, 2l/k, ...  No padding is stored.
-* Each device's local buffer is the dense C-order array of its box.
+* Each device's local buffer is the dense C-order array of its box.  The
+  paper's specs never permute dimensions; a local layout may optionally be
+  permuted (an extension for transposed layouts, not in the paper): with
+  perm = (p_0, ..., p_{n-1}), dimension k of the buffer is tensor dimension
+  p_k, i.e. the buffer is numpy.transpose(box, perm).  None is the identity.
 
 Parity pins (see tests/test_oracle_pins.py): brute-force per-element
 ownership on tiny meshes, the Fig. 2 facts stated in Section 2.2, the
@@ -132,9 +136,21 @@ def device_box(shape, mesh, dims, device):
     return tuple(box)
 
 
-def local_shape(shape, mesh, spec, device):
+def check_perm(perm, ndim):
+    """The identity for None; else perm must order 0..ndim-1."""
+    if perm is None:
+        return tuple(range(ndim))
+    perm = tuple(int(a) for a in perm)
+    if sorted(perm) != list(range(ndim)):
+        raise ValueError(f"{perm} is not a permutation of the {ndim} tensor dimensions")
+    return perm
+
+
+def local_shape(shape, mesh, spec, device, perm=None):
+    """Shape of ``device``'s buffer: its box's extents, in the order of ``perm``."""
     dims = parse_spec(spec, len(shape), len(mesh))
-    return tuple(hi - lo for lo, hi in device_box(shape, mesh, dims, device))
+    ext = tuple(hi - lo for lo, hi in device_box(shape, mesh, dims, device))
+    return tuple(ext[a] for a in check_perm(perm, len(shape)))
 
 
 def _n_devices(mesh):
@@ -158,19 +174,22 @@ def _slices(box):
 # The result of a resharding task (Section 2.2)
 # ---------------------------------------------------------------------------
 
-def shard(x, mesh, spec):
+def shard(x, mesh, spec, perm=None):
     """Lay the logical tensor ``x`` out on ``mesh`` under ``spec``.
 
-    Returns one dense C-order array per device, in row-major device order.
-    Replicated devices get equal, separate copies.
+    Returns one dense C-order array per device, in row-major device order:
+    the device's box, its dimensions ordered by ``perm``.  Replicated
+    devices get equal, separate copies.
     """
     dims = parse_spec(spec, x.ndim, len(mesh))
-    return [np.ascontiguousarray(x[_slices(device_box(x.shape, mesh, dims, d))]).copy()
+    perm = check_perm(perm, x.ndim)
+    return [np.ascontiguousarray(np.transpose(x[_slices(device_box(x.shape, mesh, dims, d))], perm)).copy()
             for d in range(_n_devices(mesh))]
 
 
-def unshard(shards, shape, mesh, spec):
-    """Rebuild the logical tensor from per-device shards.
+def unshard(shards, shape, mesh, spec, perm=None):
+    """Rebuild the logical tensor from per-device shards (buffers laid out
+    in the order of ``perm``).
 
     Every element must be covered; where replicas overlap their bits must
     agree (otherwise the input is not a valid layout and ValueError is
@@ -178,6 +197,8 @@ def unshard(shards, shape, mesh, spec):
     """
     shape = tuple(shape)
     dims = parse_spec(spec, len(shape), len(mesh))
+    perm = check_perm(perm, len(shape))
+    back = tuple(int(a) for a in np.argsort(perm))  # buffer dimension holding tensor dimension d
     if len(shards) != _n_devices(mesh):
         raise ValueError("need one shard per mesh device")
     itemsize = np.asarray(shards[0]).dtype.itemsize
@@ -187,8 +208,9 @@ def unshard(shards, shape, mesh, spec):
         box = device_box(shape, mesh, dims, d)
         want = tuple(hi - lo for lo, hi in box)
         s = _bits(np.asarray(s))
-        if s.shape != want:
-            raise ValueError(f"device {d}: shard shape {s.shape}, layout needs {want}")
+        if s.shape != tuple(want[a] for a in perm):
+            raise ValueError(f"device {d}: shard shape {s.shape}, layout needs {tuple(want[a] for a in perm)}")
+        s = np.transpose(s, back)
         sl = _slices(box)
         seen = filled[sl]
         if seen.any() and not np.array_equal(x[sl][seen], s[seen]):
@@ -200,17 +222,18 @@ def unshard(shards, shape, mesh, spec):
     return x
 
 
-def reshard(src_shards, shape, src_mesh, src_spec, dst_mesh, dst_spec):
+def reshard(src_shards, shape, src_mesh, src_spec, dst_mesh, dst_spec, src_perm=None, dst_perm=None):
     """Destination shards of one cross-mesh resharding task.
 
     Section 2.2: D, laid out on the source mesh under src_spec, is sent to
     the destination mesh where its layout becomes dst_spec.  Computed as
     unshard-then-shard on raw bits; the output arrays carry the dtype of the
-    inputs (bit-identical).
+    inputs (bit-identical).  The optional permutations order each side's
+    buffer dimensions (see the module header).
     """
     dtype = np.asarray(src_shards[0]).dtype
-    x = unshard(src_shards, shape, src_mesh, src_spec)
-    return [s.view(dtype) for s in shard(x, dst_mesh, dst_spec)]
+    x = unshard(src_shards, shape, src_mesh, src_spec, src_perm)
+    return [s.view(dtype) for s in shard(x, dst_mesh, dst_spec, dst_perm)]
 
 
 def traffic_bytes(shape, itemsize, dst_mesh, dst_spec):

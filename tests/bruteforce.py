@@ -31,8 +31,11 @@ def _owner_tables(length, k):
     return owner
 
 
-def layout(x, mesh, dims):
-    """Per-device arrays of ``x`` under (mesh, per-dim axis tuples), element by element."""
+def layout(x, mesh, dims, perm=None):
+    """Per-device arrays of ``x`` under (mesh, per-dim axis tuples), element by
+    element; with ``perm``, buffer index k is the element's rank along tensor
+    dimension perm[k]."""
+    perm = tuple(range(x.ndim)) if perm is None else tuple(perm)
     shape = x.shape
     ndev = int(np.prod(mesh))
     coords = [tuple(int(c) for c in np.unravel_index(d, mesh)) for d in range(ndev)]
@@ -52,9 +55,9 @@ def layout(x, mesh, dims):
     out = []
     for dev in range(ndev):
         per_dim = [[i for i in range(shape[d]) if holds(dev, d, i)] for d in range(len(shape))]
-        local = np.zeros(tuple(len(p) for p in per_dim), dtype=x.dtype)
+        local = np.zeros(tuple(len(per_dim[a]) for a in perm), dtype=x.dtype)
         for idx in itertools.product(*per_dim):
-            pos = tuple(tables[d][i][1] for d, i in enumerate(idx))
-            local[pos] = x[idx]
+            rank = [tables[d][i][1] for d, i in enumerate(idx)]
+            local[tuple(rank[a] for a in perm)] = x[idx]
         out.append(local)
     return out

@@ -123,6 +123,16 @@ def _parse_spec_axes_reversed(spec, ndim, mesh_ndim):
     return tuple(tuple(reversed(axes)) for axes in _PARSE(spec, ndim, mesh_ndim))
 
 
+_SHARD = R.shard
+
+
+def _shard_inverse_perm(x, mesh, spec, perm=None):
+    # the buffer laid out with the inverse permutation
+    if perm is not None:
+        perm = tuple(int(a) for a in np.argsort(perm))
+    return _SHARD(x, mesh, spec, perm)
+
+
 # scheduling across hosts (Section 3.2)
 
 def _start_times_sender_only(model, order, host):
@@ -225,6 +235,7 @@ MUTATIONS = {
     "unit_tasks_source_cuts_only": (R, "unit_tasks", _unit_tasks_source_cuts_only, _PINS_R),
     "unshard_without_replica_check": (R, "unshard", _unshard_without_replica_check, _PINS_R),
     "traffic_unique_writes": (R, "traffic_bytes", _traffic_unique_writes, _PINS_R),
+    "shard_inverse_perm": (R, "shard", _shard_inverse_perm, _PINS_R),
     "parse_spec_first_axis_only": (R, "parse_spec", _parse_spec_first_axis_only, _PINS_R),
     "parse_spec_axes_reversed": (R, "parse_spec", _parse_spec_axes_reversed, _PINS_R),
     "start_times_sender_only": (SCH, "start_times", _start_times_sender_only, _PINS_S),

@@ -7,7 +7,8 @@ a multi-axis spec token kept to its first axis or read in reverse, a
 padding-style split, the remainder on the last shards, minor-major axis
 order, column-major devices, shortest-first or heaviest-sender balancing,
 the highest-index naive sender, destination cut points dropped, no replica
-check, replicas counted once in the traffic.  Scheduling: tasks that wait
+check, replicas counted once in the traffic, a permuted buffer laid out
+with the inverse permutation.  Scheduling: tasks that wait
 for their sender host only or for every earlier task, a lower bound
 charging every candidate, shortest-first balancing, the randomized search
 left out or cut to one random order per iteration, DFS stopped at its first

@@ -406,3 +406,53 @@ def test_lpt_optimal_on_table3_cases():
 def test_naive_picks_lowest_index():
     tasks = _synthetic_tasks([5, 3], [[2, 1, 3], [4, 0]])
     assert oracle.choose_senders_naive(tasks) == [1, 0]
+
+
+# ------------------------------------------------- permuted local layouts
+
+def _perm_cases(n, seed):
+    rng = random.Random(seed)
+    out = []
+    for shape, smesh, sdims, dmesh, ddims in _brute_cases(n, seed):
+        sp = list(range(len(shape)))
+        dp = list(range(len(shape)))
+        rng.shuffle(sp)
+        rng.shuffle(dp)
+        out.append((shape, smesh, sdims, tuple(sp), dmesh, ddims, tuple(dp)))
+    return out
+
+
+@pytest.mark.parametrize("case", _perm_cases(40, 4321))
+def test_permuted_layouts_match_brute_force(case):
+    # the element-by-element formulation places each element at its rank
+    # inside the shard, read in the buffer's dimension order
+    shape, smesh, sdims, sp, dmesh, ddims, dp = case
+    x = iota(shape, np.uint16)
+    src_bf = bruteforce.layout(x, smesh, sdims, sp)
+    dst_bf = bruteforce.layout(x, dmesh, ddims, dp)
+    sspec, dspec = fmt_spec(sdims), fmt_spec(ddims)
+    for d, (a, b) in enumerate(zip(oracle.shard(x, smesh, sspec, sp), src_bf)):
+        assert a.shape == b.shape == oracle.local_shape(shape, smesh, sspec, d, sp) and np.array_equal(a, b)
+    out = oracle.reshard(src_bf, shape, smesh, sspec, dmesh, dspec, src_perm=sp, dst_perm=dp)
+    for a, b in zip(out, dst_bf):
+        assert a.shape == b.shape and np.array_equal(a, b)
+
+
+def test_permuted_layout_special_cases():
+    x = iota((5, 7), np.uint32)
+    # one device, both dimensions kept whole: the buffer is the textbook transpose
+    (t,) = oracle.shard(x, (1,), "RR", (1, 0))
+    assert t.shape == (7, 5) and all(t[j, i] == x[i, j] for i in range(5) for j in range(7))
+    # moving a tensor from the plain layout to the transposed one and back
+    there = oracle.reshard(oracle.shard(x, (2,), "S^0R"), (5, 7), (2,), "S^0R", (3,), "RS^0", dst_perm=(1, 0))
+    assert [a.shape for a in there] == [(3, 5), (2, 5), (2, 5)]
+    back = oracle.reshard(there, (5, 7), (3,), "RS^0", (2,), "S^0R", src_perm=(1, 0))
+    for a, b in zip(back, oracle.shard(x, (2,), "S^0R")):
+        assert np.array_equal(a, b)
+    # the identity permutation is the plain layout
+    for a, b in zip(oracle.shard(x, (2,), "S^0R", (0, 1)), oracle.shard(x, (2,), "S^0R")):
+        assert np.array_equal(a, b)
+    with pytest.raises(ValueError):
+        oracle.shard(x, (2,), "S^0R", (0, 0))
+    with pytest.raises(ValueError):
+        oracle.shard(x, (2,), "S^0R", (0, 1, 2))
