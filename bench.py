@@ -103,7 +103,8 @@ def main():
     ap.add_argument("--warmup", type=int, default=5)
     ap.add_argument("--config", default=None,
                     help="workload id 1..5 (default 5), uneven5 / uneven3 (workloads 5 / 3 with an uneven last "
-                         "dimension), or fanoutR (1 GiB, one sender to R replicas)")
+                         "dimension), transposed2 / transposed5 (workloads 2 / 5 with the destination stored "
+                         "[batch, hidden, seq]), or fanoutR (1 GiB, one sender to R replicas)")
     ap.add_argument("--strategy", choices=["broadcast", "sendrecv", "allgather"], default="broadcast",
                     help="broadcast (default) or a comparison strategy that re-reads slices per receiver")
     ap.add_argument("--seed", type=int, default=0)
@@ -151,14 +152,15 @@ def main():
     # (setup and check launches use 128-thread workgroups, which every kernel
     # honours, so kernel traces and counter runs tell them apart from the
     # timed launches)
-    scatter = B.reshard_plan(w.shape, w.dtype, (1,), rep, w.src_mesh, w.src_spec, block_threads=SETUP_BLOCK)
+    scatter = B.reshard_plan(w.shape, w.dtype, (1,), rep, w.src_mesh, w.src_spec, block_threads=SETUP_BLOCK,
+                             dst_perm=w.src_perm)
     src = B.empty_shards(scatter, 1)
     B.reshard_execute(scatter, [x], src)
 
     t0 = time.perf_counter()
     plan = B.reshard_plan(w.shape, w.dtype, w.src_mesh, w.src_spec, w.dst_mesh, w.dst_spec,
                           flags=flags, chunk_bytes=args.chunk_bytes, block_threads=args.block_threads,
-                          max_wgs_per_cu=args.max_wgs_per_cu)
+                          max_wgs_per_cu=args.max_wgs_per_cu, src_perm=w.src_perm, dst_perm=w.dst_perm)
     plan_us = (time.perf_counter() - t0) * 1e6
     st = B.reshard_plan_stats(plan)
     dst = B.empty_shards(plan, 1)
@@ -193,7 +195,8 @@ def main():
 
     # Round-trip check through the library: the dst of every set a step
     # wrote -> one buffer must equal x.
-    back_plan = B.reshard_plan(w.shape, w.dtype, w.dst_mesh, w.dst_spec, (1,), rep, block_threads=SETUP_BLOCK)
+    back_plan = B.reshard_plan(w.shape, w.dtype, w.dst_mesh, w.dst_spec, (1,), rep, block_threads=SETUP_BLOCK,
+                               src_perm=w.dst_perm)
     back = B.empty_shards(back_plan, 1)
     roundtrip_ok = True
     for _, d_ in sets[:min(nsets, max(args.warmup, args.steps))]:
@@ -247,9 +250,11 @@ def main():
     # the chunks of each kind the plan holds; most workloads use one).
     n_gather, n_realign = B.reshard_plan_gather_chunks(plan), B.reshard_plan_realign_chunks(plan)
     n_gather_u = B.reshard_plan_unaligned_gather_chunks(plan)
-    n_direct = st["n_descriptors"] - n_gather - n_gather_u - n_realign
+    n_transpose = B.reshard_plan_transpose_chunks(plan)
+    n_direct = st["n_descriptors"] - n_gather - n_gather_u - n_transpose - n_realign
     kernel = max((n_direct, "reshard_kernel"), (n_gather, "reshard_gather_kernel"),
-                 (n_gather_u, "reshard_gather_u_kernel"), (n_realign, "reshard_realign_kernel"))[1]
+                 (n_gather_u, "reshard_gather_u_kernel"), (n_transpose, "reshard_transpose_kernel"),
+                 (n_realign, "reshard_realign_kernel"))[1]
     out = {
         "metric": METRIC,
         "value": round(gbs, 2),
@@ -272,7 +277,7 @@ def main():
         },
         "pct_of_hbm_peak": round(100.0 * gbs / HBM_PEAK_GBS, 2),
         "roofline": {
-            "kernel": kernel, "launches_per_step": sum(1 for n in (n_direct, n_gather, n_gather_u, n_realign) if n)
+            "kernel": kernel, "launches_per_step": sum(1 for n in (n_direct, n_gather, n_gather_u, n_transpose, n_realign) if n)
                                                         + (args.strategy == "allgather" and n_direct > 0),
             "bound": "hbm", "achieved": round(gbs, 2), "peak": HBM_PEAK_GBS, "unit": "GB/s",
             "frac": round(gbs / HBM_PEAK_GBS, 4), "traffic": traffic,

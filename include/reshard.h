@@ -158,6 +158,30 @@ reshard_status_t reshard_plan_ex(int ndim, const int64_t *shape, reshard_dtype_t
                                  reshard_plan_t **out);
 
 /*
+ * As reshard_plan_ex, with permuted local layouts on either side: the buffer
+ * of every source (destination) device holds its shard with its dimensions
+ * in the order src_perm (dst_perm) -- buffer dimension k is tensor
+ * dimension perm[k], so the buffer is numpy.transpose(shard, perm) in dense
+ * C order -- and reshard_plan_local_shape reports that order.  NULL is the
+ * identity (the layout of reshard_plan).  The paper's sharding specs never
+ * permute dimensions (Section 2.2, "Sharding spec"); this lets a reshard
+ * also change the memory order of the tensor, e.g. [batch, seq, hidden] on
+ * one side and [batch, hidden, seq] on the other.  Where the two sides are
+ * contiguous along different tensor dimensions, tiles are transposed
+ * through LDS (reshard_plan_transpose_chunks).
+ *
+ * perm arrays have ndim entries and are read during the call only.
+ * Errors: those of reshard_plan_ex; EINVAL when a permutation does not
+ * order 0..ndim-1; EUNSUPPORTED for a comparison-strategy flag with a
+ * permuted layout.
+ */
+reshard_status_t reshard_plan_permuted(int ndim, const int64_t *shape, reshard_dtype_t dtype,
+                                       int src_mesh_ndim, const int64_t *src_mesh, const char *src_spec,
+                                       const int32_t *src_perm, int dst_mesh_ndim, const int64_t *dst_mesh,
+                                       const char *dst_spec, const int32_t *dst_perm, unsigned flags,
+                                       const reshard_tuning_t *tuning, reshard_plan_t **out);
+
+/*
  * Upload the plan's descriptor, receiver and segment tables to the current
  * HIP device (one hipMalloc + synchronous copies; nothing if already done
  * on that device).  After it, reshard_execute on that device allocates and
@@ -276,6 +300,11 @@ int64_t reshard_plan_gather_chunks(const reshard_plan_t *plan);
  * byte alignment (uneven splits, rows in different 16-byte phases;
  * RESHARD_NO_GATHER turns them off), or -1 for a NULL plan. */
 int64_t reshard_plan_unaligned_gather_chunks(const reshard_plan_t *plan);
+
+/* Number of workgroup chunks that transpose tiles through LDS (tasks whose
+ * source and destination layouts are contiguous along different tensor
+ * dimensions), or -1 for a NULL plan. */
+int64_t reshard_plan_transpose_chunks(const reshard_plan_t *plan);
 
 /*
  * Unit task `index` (0 <= index < n_unit_tasks), in lexicographic order of the

@@ -71,6 +71,13 @@ def load(path=None):
     lib.reshard_plan.argtypes = plan_args + [ctypes.POINTER(ctypes.c_void_p)]
     lib.reshard_plan.restype = ctypes.c_int
     lib.reshard_plan_ex.argtypes = plan_args + [ctypes.POINTER(reshard_tuning_t), ctypes.POINTER(ctypes.c_void_p)]
+    _I32P = ctypes.POINTER(ctypes.c_int32)
+    lib.reshard_plan_permuted.argtypes = [ctypes.c_int, _I64P, ctypes.c_int, ctypes.c_int, _I64P, ctypes.c_char_p,
+                                          _I32P, ctypes.c_int, _I64P, ctypes.c_char_p, _I32P, ctypes.c_uint,
+                                          ctypes.POINTER(reshard_tuning_t), ctypes.POINTER(ctypes.c_void_p)]
+    lib.reshard_plan_permuted.restype = ctypes.c_int
+    lib.reshard_plan_transpose_chunks.argtypes = [ctypes.c_void_p]
+    lib.reshard_plan_transpose_chunks.restype = ctypes.c_int64
     lib.reshard_plan_ex.restype = ctypes.c_int
     lib.reshard_execute.argtypes = [ctypes.c_void_p, _VPP, _VPP, ctypes.c_void_p]
     lib.reshard_execute.restype = ctypes.c_int
@@ -186,12 +193,23 @@ class Plan:
 
 
 def reshard_plan(shape, dtype, src_mesh, src_spec, dst_mesh, dst_spec, flags=0,
-                 chunk_bytes=0, block_threads=0, max_wgs_per_cu=0, gather_band=0):
+                 chunk_bytes=0, block_threads=0, max_wgs_per_cu=0, gather_band=0, src_perm=None, dst_perm=None):
+    """A plan; src_perm / dst_perm (tuples or None) permute each side's local
+    buffer layout (buffer dimension k is tensor dimension perm[k])."""
     lib = load()
     h = ctypes.c_void_p()
     args = [len(shape), _i64(shape), _dtype_code(dtype), len(src_mesh), _i64(src_mesh),
             src_spec.encode(), len(dst_mesh), _i64(dst_mesh), dst_spec.encode(), int(flags)]
-    if chunk_bytes or block_threads or max_wgs_per_cu or gather_band:
+    if src_perm is not None or dst_perm is not None:
+        def perm(p):
+            return None if p is None else (ctypes.c_int32 * max(1, len(p)))(*[int(a) for a in p])
+        t = reshard_tuning_t(chunk_bytes=int(chunk_bytes), block_threads=int(block_threads),
+                             max_wgs_per_cu=int(max_wgs_per_cu), gather_band=int(gather_band))
+        _check(lib.reshard_plan_permuted(len(shape), _i64(shape), _dtype_code(dtype), len(src_mesh), _i64(src_mesh),
+                                         src_spec.encode(), perm(src_perm), len(dst_mesh), _i64(dst_mesh),
+                                         dst_spec.encode(), perm(dst_perm), int(flags), ctypes.byref(t),
+                                         ctypes.byref(h)))
+    elif chunk_bytes or block_threads or max_wgs_per_cu or gather_band:
         t = reshard_tuning_t(chunk_bytes=int(chunk_bytes), block_threads=int(block_threads),
                              max_wgs_per_cu=int(max_wgs_per_cu), gather_band=int(gather_band))
         _check(lib.reshard_plan_ex(*args, ctypes.byref(t), ctypes.byref(h)))
@@ -277,6 +295,10 @@ def reshard_plan_gather_chunks(plan):
 
 def reshard_plan_realign_chunks(plan):
     return int(load().reshard_plan_realign_chunks(plan.handle))
+
+
+def reshard_plan_transpose_chunks(plan):
+    return load().reshard_plan_transpose_chunks(plan.handle)
 
 
 def reshard_plan_unaligned_gather_chunks(plan):

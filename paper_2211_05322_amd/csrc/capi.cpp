@@ -71,9 +71,25 @@ reshard_status_t check_mesh(const char *side, int mesh_ndim, const int64_t *mesh
     return RESHARD_OK;
 }
 
+// A layout permutation: NULL (identity) or an ordering of 0..ndim-1.
+reshard_status_t check_perm(const char *side, const int32_t *perm, int ndim, std::vector<int> &out) {
+    out.resize(size_t(ndim));
+    std::vector<char> seen(size_t(ndim), 0);
+    for (int k = 0; k < ndim; ++k) {
+        const int a = perm ? int(perm[k]) : k;
+        if (a < 0 || a >= ndim || seen[size_t(a)])
+            return fail(RESHARD_EINVAL, std::string(side) + " permutation is not an ordering of the " +
+                                            std::to_string(ndim) + " tensor dimensions");
+        seen[size_t(a)] = 1;
+        out[size_t(k)] = a;
+    }
+    return RESHARD_OK;
+}
+
 reshard_status_t make_plan(int ndim, const int64_t *shape, reshard_dtype_t dtype, int smn, const int64_t *sm,
                            const char *sspec, int dmn, const int64_t *dm, const char *dspec, unsigned flags,
-                           const reshard_tuning_t *tuning, reshard_plan_t **out) {
+                           const reshard_tuning_t *tuning, reshard_plan_t **out, const int32_t *sperm = nullptr,
+                           const int32_t *dperm = nullptr) {
     if (!out) return fail(RESHARD_EINVAL, "out is NULL");
     *out = nullptr;
     if (ndim < 1 || ndim > RESHARD_MAX_NDIM)
@@ -129,6 +145,15 @@ reshard_status_t make_plan(int ndim, const int64_t *shape, reshard_dtype_t dtype
     if (!err.empty()) return fail(RESHARD_EINVAL, "source " + err);
     err = rs::parse_spec(dspec, ndim, dmn, dax);
     if (!err.empty()) return fail(RESHARD_EINVAL, "destination " + err);
+    std::vector<int> sp, dp;
+    st = check_perm("source", sperm, ndim, sp);
+    if (st != RESHARD_OK) return st;
+    st = check_perm("destination", dperm, ndim, dp);
+    if (st != RESHARD_OK) return st;
+    bool permuted = false;
+    for (int k = 0; k < ndim; ++k) permuted = permuted || sp[size_t(k)] != k || dp[size_t(k)] != k;
+    if (permuted && (flags & (RESHARD_STRATEGY_SENDRECV | RESHARD_STRATEGY_ALLGATHER)))
+        return fail(RESHARD_EUNSUPPORTED, "the comparison strategies take unpermuted layouts only");
 
     rs::Plan *p = new (std::nothrow) rs::Plan();
     if (!p) return fail(RESHARD_ENOMEM, "out of host memory");
@@ -138,6 +163,8 @@ reshard_status_t make_plan(int ndim, const int64_t *shape, reshard_dtype_t dtype
         p->es = es;
         p->flags = flags;
         p->tuning = tn;
+        p->sperm = sp;
+        p->dperm = dp;
         rs::build_layout(p->shape, std::vector<int64_t>(sm, sm + smn), sax, p->src);
         rs::build_layout(p->shape, std::vector<int64_t>(dm, dm + dmn), dax, p->dst);
         // bound the number of unit tasks before enumerating them
@@ -185,6 +212,17 @@ reshard_status_t reshard_plan_ex(int ndim, const int64_t *shape, reshard_dtype_t
     return rs::guarded([&]() -> reshard_status_t {
         return make_plan(ndim, shape, dtype, src_mesh_ndim, src_mesh, src_spec, dst_mesh_ndim, dst_mesh, dst_spec,
                          flags, tuning, out);
+    });
+}
+
+reshard_status_t reshard_plan_permuted(int ndim, const int64_t *shape, reshard_dtype_t dtype, int src_mesh_ndim,
+                                       const int64_t *src_mesh, const char *src_spec, const int32_t *src_perm,
+                                       int dst_mesh_ndim, const int64_t *dst_mesh, const char *dst_spec,
+                                       const int32_t *dst_perm, unsigned flags, const reshard_tuning_t *tuning,
+                                       reshard_plan_t **out) {
+    return rs::guarded([&]() -> reshard_status_t {
+        return make_plan(ndim, shape, dtype, src_mesh_ndim, src_mesh, src_spec, dst_mesh_ndim, dst_mesh, dst_spec,
+                         flags, tuning, out, src_perm, dst_perm);
     });
 }
 
@@ -244,7 +282,12 @@ int64_t reshard_plan_gather_chunks(const reshard_plan_t *plan) {
 
 int64_t reshard_plan_realign_chunks(const reshard_plan_t *plan) {
     const rs::Plan *p = as_plan(plan);
-    return p ? int64_t(p->descs.size() - p->n_direct - p->n_gather - p->n_gather_u) : -1;
+    return p ? int64_t(p->descs.size() - p->n_direct - p->n_gather - p->n_gather_u - p->n_transpose) : -1;
+}
+
+int64_t reshard_plan_transpose_chunks(const reshard_plan_t *plan) {
+    const rs::Plan *p = as_plan(plan);
+    return p ? int64_t(p->n_transpose) : -1;
 }
 
 int64_t reshard_plan_unaligned_gather_chunks(const reshard_plan_t *plan) {
@@ -295,6 +338,64 @@ reshard_status_t reshard_debug_execute_host(const reshard_plan_t *plan, void *co
             const rs::Desc &d = p->descs[di];
             const uint32_t w = 1u << rs::kind_log2w(d.kind);
             const uint32_t levels = rs::kind_levels(d.kind);
+            const size_t t0 = p->n_direct + p->n_gather + p->n_gather_u;
+            if (di >= t0 && di < t0 + p->n_transpose) {
+                // tile-transpose chunk: the kernel's tile arithmetic and
+                // swizzled LDS tile, every access bounds-checked
+                const uint32_t es = uint32_t(p->es), te = rs::tile_elems(es), vpe = 16u / es;
+                const bool ald = (d.kind & rs::kTAlignLoad) != 0, ast = (d.kind & rs::kTAlignStore) != 0;
+                if ((1u << (d.kind & 0xFu)) != es) return fail(RESHARD_EINVAL, "internal: transpose element size");
+                const uint64_t sbytes = uint64_t(p->src_local_numel[d.src_buf] * p->es);
+                lds.assign(te * rs::kTileBytes, 0);
+                for (uint32_t t = d.v0; t < d.v1; ++t) {
+                    const rs::TileAt at = rs::tile_offsets(d, t, es);
+                    const uint32_t na = std::min(te, d.run - at.ta * te), nb = std::min(te, d.batch - at.tb * te);
+                    for (uint32_t i = 0; i < te * 8u; ++i) {  // load phase
+                        const uint32_t r = i >> 3, c = i & 7u;
+                        if (r >= nb) continue;
+                        const uint32_t a0 = c * vpe;
+                        const uint32_t nv = a0 < na ? std::min(vpe, na - a0) : 0u;
+                        uint8_t x[16] = {0};
+                        const uint64_t q = d.src_base + uint32_t(at.src + r * d.ss[0] + c * 16u);
+                        if (nv == vpe && ald) {
+                            if (q % 16 != 0) return fail(RESHARD_EINVAL, "internal: transpose vector load misaligned");
+                            if (q + 16 > sbytes) return fail(RESHARD_EINVAL, "internal: transpose load outside its source shard");
+                            std::memcpy(x, static_cast<const char *>(src_ptrs[d.src_buf]) + q, 16);
+                        } else {
+                            for (uint32_t e = 0; e < nv; ++e) {
+                                if (q + (e + 1) * es > sbytes) return fail(RESHARD_EINVAL, "internal: transpose load outside its source shard");
+                                std::memcpy(x + e * es, static_cast<const char *>(src_ptrs[d.src_buf]) + q + e * es, es);
+                            }
+                        }
+                        const uint32_t o = rs::tile_lds(r, c, 0, es);
+                        if (o + 16 > lds.size()) return fail(RESHARD_EINVAL, "internal: transpose LDS write out of range");
+                        std::memcpy(lds.data() + o, x, 16);
+                    }
+                    for (uint32_t i = 0; i < te * 8u; ++i) {  // store phase
+                        const uint32_t a = i >> 3, j = i & 7u;
+                        if (a >= na) continue;
+                        const uint32_t b0 = j * vpe;
+                        const uint32_t nv = b0 < nb ? std::min(vpe, nb - b0) : 0u;
+                        if (nv == 0) continue;
+                        uint8_t y[16] = {0};
+                        for (uint32_t e = 0; e < vpe; ++e) {
+                            const uint32_t o = rs::tile_lds(b0 + e, (a * es) >> 4, (a * es) & 15u, es);
+                            if (o + es > lds.size()) return fail(RESHARD_EINVAL, "internal: transpose LDS read out of range");
+                            std::memcpy(y + e * es, lds.data() + o, es);
+                        }
+                        for (uint32_t r = 0; r < d.nfan; ++r) {
+                            const int32_t dev = p->fan[d.fan_off + r];
+                            const uint64_t dbytes = uint64_t(p->dst_local_numel[dev] * p->es);
+                            const uint64_t q = d.dst_base + uint32_t(at.dst + a * d.ds[0] + j * 16u);
+                            if (nv == vpe && ast && q % 16 != 0)
+                                return fail(RESHARD_EINVAL, "internal: transpose vector store misaligned");
+                            if (q + nv * es > dbytes) return fail(RESHARD_EINVAL, "internal: transpose store outside its destination shard");
+                            std::memcpy(static_cast<char *>(dst_ptrs[dev]) + q, y, nv * es);
+                        }
+                    }
+                }
+                continue;
+            }
             if (di >= p->n_direct + p->n_gather && di < p->n_direct + p->n_gather + p->n_gather_u) {
                 // unaligned row-gather chunk: the kernel's slot -> pieces arithmetic
                 const uint32_t rb = d.vpr, ns = d.pad[1];
@@ -484,12 +585,19 @@ reshard_status_t reshard_debug_execute_host(const reshard_plan_t *plan, void *co
                 }
                 continue;
             }
+            const uint64_t sbytes = uint64_t(
+                (sbuf < p->src.ndev ? p->src_local_numel[sbuf] : p->dst_local_numel[sbuf - p->src.ndev]) * p->es);
             for (uint32_t v = d.v0; v < d.v1; ++v) {
                 const rs::Rel o = levels == 1   ? rs::chunk_offsets<1>(d, v, w)
                                   : levels == 2 ? rs::chunk_offsets<2>(d, v, w)
                                                 : rs::chunk_offsets<3>(d, v, w);
+                if (d.src_base + o.src + w > sbytes)
+                    return fail(RESHARD_EINVAL, "internal: load outside its source shard");
                 for (uint32_t r = 0; r < d.nfan; ++r) {
-                    char *dst = static_cast<char *>(dst_ptrs[p->fan[d.fan_off + r]]) + d.dst_base;
+                    const int32_t dev = p->fan[d.fan_off + r];
+                    if (d.dst_base + o.dst + w > uint64_t(p->dst_local_numel[dev] * p->es))
+                        return fail(RESHARD_EINVAL, "internal: store outside its destination shard");
+                    char *dst = static_cast<char *>(dst_ptrs[dev]) + d.dst_base;
                     std::memcpy(dst + o.dst, src + o.src, w);
                 }
             }

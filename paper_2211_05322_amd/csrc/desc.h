@@ -132,6 +132,54 @@ struct Seg {
 static_assert(sizeof(Seg) == 32, "segment entries are shared by host and device");
 constexpr uint32_t kMaxSegs = 256;  // segment entries one gather chunk may stage
 
+// Tile-transpose path (own section and kernel), for tasks whose source and
+// destination layouts are contiguous along different tensor dimensions (a
+// permuted local layout): A is the dimension contiguous in the sender's
+// buffer, B the one contiguous in the receivers'.  A tile is kTileBytes /
+// es elements along each of A and B: its rows (one per B index) are
+// kTileBytes contiguous source bytes, its columns (one per A index)
+// kTileBytes contiguous destination bytes.  A chunk is a range of tiles of a
+// piece (tile t: tb = t mod ntb fastest, then ta, then the outer levels o1,
+// o2).  Fields: kind = log2 es | kTAlignLoad | kTAlignStore; ss[0] = sender
+// stride of B, ds[0] = receiver stride of A; ss[1], ds[1] and ss[2], ds[2]
+// the outer levels o1 (inner) and o2; vpr = ntb, n1 = nta, n2 = extent of o1
+// (with their fast divisions); run = extent of A, batch = extent of B
+// (elements); v0, v1 the tiles; src_base/dst_base, src_rel0/dst_rel0 as
+// usual, for tile v0's origin.  The aligned flags say that every tile row
+// (column) starts on a 16-byte boundary, so whole 16-byte vectors of it are
+// loaded (stored) at once; otherwise elements move one by one.
+constexpr uint32_t kTileBytes = 128;
+constexpr uint32_t kTAlignLoad = 0x10u;
+constexpr uint32_t kTAlignStore = 0x20u;
+constexpr uint32_t tile_elems(uint32_t es) { return kTileBytes / es; }
+
+// Relative offsets (sender, receiver) of tile t's origin from the chunk's
+// first tile (mod 2^32), and the tile's (ta, tb) indices.
+struct TileAt {
+    uint32_t src, dst, ta, tb;
+};
+
+constexpr TileAt tile_offsets(const Desc &d, uint32_t t, uint32_t es) {
+    const uint32_t r = fastdiv(t, d.mul_vpr, d.sh_vpr);
+    const uint32_t tb = t - r * d.vpr;
+    const uint32_t o = fastdiv(r, d.mul_n1, d.sh_n1);
+    const uint32_t ta = r - o * d.n1;
+    const uint32_t o2 = fastdiv(o, d.mul_n2, d.sh_n2);
+    const uint32_t o1 = o - o2 * d.n2;
+    const uint32_t te = tile_elems(es);
+    const uint32_t s = tb * te * d.ss[0] + ta * kTileBytes + o1 * d.ss[1] + o2 * d.ss[2];
+    const uint32_t u = ta * te * d.ds[0] + tb * kTileBytes + o1 * d.ds[1] + o2 * d.ds[2];
+    return TileAt{s - d.src_rel0, u - d.dst_rel0, ta, tb};
+}
+
+// LDS byte offset of byte `o` of 16-byte column slot c in tile row r: rows
+// are kTileBytes apart, and the slot is XOR-swizzled by the row's group of
+// 16 / es rows, so the column reads of the store phase (16 / es rows of one
+// slot per output vector, 8 output vectors per wave) hit distinct banks.
+constexpr uint32_t tile_lds(uint32_t r, uint32_t c, uint32_t o, uint32_t es) {
+    return r * kTileBytes + ((c ^ ((r / (16u / es)) & 7u)) << 4) + o;
+}
+
 // Outer-level indices of a row (level 1 = innermost outer level).
 template <int LEVELS>
 constexpr void row_indices(const Desc &d, uint32_t row, uint32_t &i1, uint32_t &i2, uint32_t &i3) {

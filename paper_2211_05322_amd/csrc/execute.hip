@@ -780,6 +780,163 @@ __global__ __launch_bounds__(256) void reshard_gather_u_kernel(KArgs<NPTR> args)
     }
 }
 
+// Tile transpose (see desc.h): per tile, a load phase (rows of the tile,
+// contiguous in the sender's buffer, into LDS: 16-byte vectors where the
+// rows are aligned, else element by element) and a store phase (columns of
+// the tile, contiguous in the receivers' buffers: each lane assembles one
+// 16-byte vector from 16 / ES rows of one column and stores it to every
+// receiver).  Lanes 8k .. 8k + 7 cover one row (one column) of 128 bytes,
+// so a wave moves 8 whole cache lines per instruction on both sides.
+template <int ES>
+__device__ __forceinline__ void tile_put(unsigned char *lds, uint32_t off, u32x4 v) {
+    *reinterpret_cast<u32x4 *>(lds + off) = v;
+}
+
+template <int ES>
+__device__ __forceinline__ u32x4 tile_column(const unsigned char *lds, uint32_t b0, uint32_t a) {
+    const uint32_t c = (a * ES) >> 4, o = (a * ES) & 15u;
+    if constexpr (ES == 8) {
+        u32x4 y;
+        const u32x2 lo = *reinterpret_cast<const u32x2 *>(lds + tile_lds(b0, c, o, ES));
+        const u32x2 hi = *reinterpret_cast<const u32x2 *>(lds + tile_lds(b0 + 1, c, o, ES));
+        y.x = lo.x; y.y = lo.y; y.z = hi.x; y.w = hi.y;
+        return y;
+    } else if constexpr (ES == 4) {
+        u32x4 y;
+        y.x = *reinterpret_cast<const uint32_t *>(lds + tile_lds(b0, c, o, ES));
+        y.y = *reinterpret_cast<const uint32_t *>(lds + tile_lds(b0 + 1, c, o, ES));
+        y.z = *reinterpret_cast<const uint32_t *>(lds + tile_lds(b0 + 2, c, o, ES));
+        y.w = *reinterpret_cast<const uint32_t *>(lds + tile_lds(b0 + 3, c, o, ES));
+        return y;
+    } else {
+        uint32_t w[4];
+#pragma unroll
+        for (uint32_t q = 0; q < 4; ++q) {
+            uint32_t acc = 0;
+#pragma unroll
+            for (uint32_t e = 0; e < 4 / ES; ++e) {
+                const uint32_t r = b0 + q * (4 / ES) + e;
+                uint32_t x;
+                if constexpr (ES == 2) x = *reinterpret_cast<const uint16_t *>(lds + tile_lds(r, c, o, ES));
+                else x = lds[tile_lds(r, c, o, ES)];
+                acc |= x << (8u * ES * e);
+            }
+            w[q] = acc;
+        }
+        u32x4 y;
+        y.x = w[0]; y.y = w[1]; y.z = w[2]; y.w = w[3];
+        return y;
+    }
+}
+
+template <int ES> struct Elem;
+template <> struct Elem<1> { typedef unsigned char T; };
+template <> struct Elem<2> { typedef unsigned short T; };
+template <> struct Elem<4> { typedef unsigned int T; };
+template <> struct Elem<8> { typedef unsigned long long T; };
+
+// The first n (< 16 / ES) elements at q, one load each, packed into a
+// 16-byte value (the rest zero).  Unrolled with constant indices, so the
+// value stays in registers.
+template <int ES>
+__device__ __forceinline__ u32x4 load_elems(const RS_GLOBAL unsigned char *q, uint32_t n) {
+    typedef typename Elem<ES>::T E;
+    uint32_t w[4] = {0u, 0u, 0u, 0u};
+#pragma unroll
+    for (uint32_t e = 0; e < 16u / ES; ++e) {
+        if (e < n) {
+            const E v = ((const RS_GLOBAL E *)q)[e];
+            if constexpr (ES == 8) {
+                w[2 * e] = uint32_t(v);
+                w[2 * e + 1] = uint32_t(uint64_t(v) >> 32);
+            } else {
+                w[(e * ES) / 4] |= uint32_t(v) << (8u * ((e * ES) % 4));
+            }
+        }
+    }
+    u32x4 x;
+    x.x = w[0]; x.y = w[1]; x.z = w[2]; x.w = w[3];
+    return x;
+}
+
+// Store the first n (< 16 / ES) elements of y at q, one store each.
+template <int ES>
+__device__ __forceinline__ void store_elems(RS_GLOBAL unsigned char *q, u32x4 y, uint32_t n) {
+    typedef typename Elem<ES>::T E;
+    const uint32_t w[4] = {y.x, y.y, y.z, y.w};
+#pragma unroll
+    for (uint32_t e = 0; e < 16u / ES; ++e) {
+        if (e < n) {
+            E v;
+            if constexpr (ES == 8) v = E(w[2 * e]) | (E(w[2 * e + 1]) << 32);
+            else v = E(w[(e * ES) / 4] >> (8u * ((e * ES) % 4)));
+            ((RS_GLOBAL E *)q)[e] = v;
+        }
+    }
+}
+
+template <int ES, int NPTR>
+__device__ __forceinline__ void run_transpose(const Desc &d, const RS_CONST KArgs<NPTR> *a) {
+    constexpr uint32_t T = kTileBytes / ES, V = 16u / ES;
+    unsigned char *lds = rs_lds;
+    const RS_GLOBAL unsigned char *src = (const RS_GLOBAL unsigned char *)a->ptr[d.src_buf] + d.src_base;
+    const RS_CONST int32_t *fan = (const RS_CONST int32_t *)(a->fan + d.fan_off);
+    const bool ald = (d.kind & kTAlignLoad) != 0, ast = (d.kind & kTAlignStore) != 0;
+    const uint32_t nthr = blockDim.x, tid = threadIdx.x;
+    for (uint32_t t = d.v0; t < d.v1; ++t) {
+        const TileAt at = tile_offsets(d, t, ES);
+        const uint32_t na = d.run - at.ta * T < T ? d.run - at.ta * T : T;
+        const uint32_t nb = d.batch - at.tb * T < T ? d.batch - at.tb * T : T;
+        for (uint32_t i = tid; i < T * 8u; i += nthr) {
+            const uint32_t r = i >> 3, c = i & 7u;
+            if (r >= nb) continue;
+            const uint32_t a0 = c * V;
+            const uint32_t nv = a0 < na ? (na - a0 < V ? na - a0 : V) : 0u;
+            const RS_GLOBAL unsigned char *q = src + (at.src + r * d.ss[0] + c * 16u);
+            u32x4 x;
+            if (nv == V && ald) x = load_vec((const RS_GLOBAL u32x4 *)q);
+            else x = load_elems<ES>(q, nv);
+            tile_put<ES>(lds, tile_lds(r, c, 0, ES), x);
+        }
+        __syncthreads();
+        for (uint32_t i = tid; i < T * 8u; i += nthr) {
+            const uint32_t aa = i >> 3, j = i & 7u;
+            if (aa >= na) continue;
+            const uint32_t b0 = j * V;
+            const uint32_t nv = b0 < nb ? (nb - b0 < V ? nb - b0 : V) : 0u;
+            if (nv == 0) continue;
+            const u32x4 y = tile_column<ES>(lds, b0, aa);
+            const uint32_t off = at.dst + aa * d.ds[0] + j * 16u;
+            if (nv == V && ast) {
+                for (uint32_t r = 0; r < d.nfan; ++r) {
+                    RS_GLOBAL char *dst = (RS_GLOBAL char *)a->ptr[a->nsrc + uint32_t(fan[r])] + d.dst_base;
+                    store_vec((RS_GLOBAL u32x4 *)(dst + off), y);
+                }
+            } else {
+                for (uint32_t r = 0; r < d.nfan; ++r)
+                    store_elems<ES>((RS_GLOBAL unsigned char *)a->ptr[a->nsrc + uint32_t(fan[r])] + d.dst_base + off,
+                                    y, nv);
+            }
+        }
+        __syncthreads();
+    }
+}
+
+template <int NPTR>
+__global__ __launch_bounds__(256) void reshard_transpose_kernel(KArgs<NPTR> args) {
+    const RS_CONST KArgs<NPTR> *a = (const RS_CONST KArgs<NPTR> *)__builtin_amdgcn_kernarg_segment_ptr();
+    const uint32_t b = blockIdx.x;
+    const uint32_t idx = a->per_xcd ? (b & 7u) * a->per_xcd + (b >> 3) : b;
+    if (idx >= a->ndesc) return;
+    const Desc d = load_desc(a, idx);
+    switch (d.kind & 0xFu) {
+        case 0: run_transpose<1>(d, a); break;
+        case 1: run_transpose<2>(d, a); break;
+        case 2: run_transpose<4>(d, a); break;
+        default: run_transpose<8>(d, a); break;
+    }
+}
+
 // Realignment chunks run in their own kernel so their register use does not
 // bound the direct kernel's occupancy.  STAGE: through LDS, else shifted loads.
 template <int NPTR, bool STAGE>
@@ -914,7 +1071,8 @@ reshard_status_t launch(const Plan &p, const Desc *descs, const int32_t *fan, co
         p.tuning.cap_is_default ? residency_lds(p.direct_fanout <= 2 ? 16u : 8u, dblock) : user_lds;
     const uint32_t n_direct = uint32_t(p.n_direct), n_gather = uint32_t(p.n_gather);
     const uint32_t n_gather_u = uint32_t(p.n_gather_u);
-    const uint32_t n_realign = uint32_t(p.descs.size() - p.n_direct - p.n_gather - p.n_gather_u);
+    const uint32_t n_transpose = uint32_t(p.n_transpose);
+    const uint32_t n_realign = uint32_t(p.descs.size() - p.n_direct - p.n_gather - p.n_gather_u - p.n_transpose);
     const uint32_t n_phase1 = uint32_t(p.n_phase1);
     if (n_phase1) {
         const reshard_status_t st = launch_one(reshard_kernel<NPTR>, a, n_phase1, remap, dblock, cap_lds, stream);
@@ -958,8 +1116,18 @@ reshard_status_t launch(const Plan &p, const Desc *descs, const int32_t *fan, co
                                                ulds > kGatherULds ? ulds : kGatherULds, stream, 8u * kUGroup);
         if (st != RESHARD_OK) return st;
     }
-    if (n_realign) {
+    if (n_transpose) {
+        // the tile (kTileBytes rows of kTileBytes / es elements) in LDS;
+        // no residency cap
         a.descs = descs + n_direct + n_gather + n_gather_u;
+        const uint32_t tblock = block < 256u ? block : 256u;
+        const uint32_t lds = (kTileBytes / uint32_t(p.es)) * kTileBytes;
+        const reshard_status_t st =
+            launch_one(reshard_transpose_kernel<NPTR>, a, n_transpose, remap, tblock, lds, stream);
+        if (st != RESHARD_OK) return st;
+    }
+    if (n_realign) {
+        a.descs = descs + n_direct + n_gather + n_gather_u + n_transpose;
         // Realignment kernels hide their load -> shift -> store latency with
         // resident workgroups: no residency cap (measured: capping at 12
         // waves per CU halves their throughput).  Staging takes its LDS.

@@ -243,6 +243,33 @@ std::pair<uint64_t, uint64_t> piece_off64(const Piece &pc, uint64_t vpr, uint64_
 
 constexpr uint64_t kMaxChunkSpan = uint64_t(1) << 32;
 
+// Byte extents (end of the last byte from the origin) of a piece on the two
+// sides.
+std::pair<uint64_t, uint64_t> piece_span(const Piece &pc) {
+    uint64_t es_ = uint64_t(pc.run), ed = uint64_t(pc.run);
+    for (const auto &l : pc.outer) {
+        es_ += uint64_t(l.n - 1) * uint64_t(l.ss);
+        ed += uint64_t(l.n - 1) * uint64_t(l.ds);
+    }
+    return {es_, ed};
+}
+
+// Whether offsets grow with the vector index on both sides: every level's
+// stride is at least the extent of everything inside it.  Plain (unpermuted)
+// layouts always are; a permuted one need not be, and its chunks then take
+// the piece's origin as their base (every offset of a piece is at or above
+// its origin, strides being non-negative).
+bool monotone(const Piece &pc) {
+    uint64_t es_ = uint64_t(pc.run), ed = uint64_t(pc.run);
+    for (size_t i = pc.outer.size(); i-- > 0;) {
+        const Level &l = pc.outer[i];
+        if (uint64_t(l.ss) < es_ || uint64_t(l.ds) < ed) return false;
+        es_ += uint64_t(l.n - 1) * uint64_t(l.ss);
+        ed += uint64_t(l.n - 1) * uint64_t(l.ds);
+    }
+    return true;
+}
+
 // Realignment path: chunks are ranges of whole rows.
 void emit_realign(Plan &p, const Piece &pc, int32_t src_buf, int64_t fan_off, int64_t nfan, int64_t chunk_bytes) {
     Desc d{};
@@ -274,10 +301,11 @@ void emit_realign(Plan &p, const Piece &pc, int32_t src_buf, int64_t fan_off, in
         p.too_many = true;
         return;
     }
+    const bool mono = monotone(pc);
     for (uint64_t r0 = 0; r0 < rows;) {
         uint64_t r1 = std::min(rows, r0 + cr);
-        const auto first = piece_off64(pc, 1, r0);
-        for (;;) {  // spans below 2^31: the kernel forms signed 32-bit word offsets
+        const auto first = mono ? piece_off64(pc, 1, r0) : std::pair<uint64_t, uint64_t>(pc.src_off, pc.dst_off);
+        for (; mono;) {  // spans below 2^31: the kernel forms signed 32-bit word offsets
             const auto last = piece_off64(pc, 1, r1 - 1);
             if (last.first + uint64_t(pc.run) - first.first < kMaxChunkSpan / 2 &&
                 last.second + uint64_t(pc.run) - first.second < kMaxChunkSpan / 2)
@@ -342,10 +370,11 @@ void emit(Plan &p, const Piece &pc, int32_t src_buf, int64_t fan_off, int64_t nf
         p.too_many = true;
         return;
     }
+    const bool mono = monotone(pc);
     for (uint64_t v0 = 0; v0 < total;) {
         uint64_t v1 = std::min(total, v0 + cv);
-        const auto first = piece_off64(pc, vpr, v0);
-        for (;;) {  // shrink until the chunk spans < 2^32 bytes on both sides
+        const auto first = mono ? piece_off64(pc, vpr, v0) : std::pair<uint64_t, uint64_t>(pc.src_off, pc.dst_off);
+        for (; mono;) {  // shrink until the chunk spans < 2^32 bytes on both sides
             const auto last = piece_off64(pc, vpr, v1 - 1);
             if (last.first + uint64_t(pc.w) - first.first < kMaxChunkSpan &&
                 last.second + uint64_t(pc.w) - first.second < kMaxChunkSpan)
@@ -390,6 +419,16 @@ void split_emit(Plan &p, Piece pc, int32_t src_buf, int64_t fan_off, int64_t nfa
         peel_top(p, pc, src_buf, fan_off, nfan, chunk_bytes);
         return;
     }
+    if (!monotone(pc)) {
+        // chunks based at the piece's origin: the whole piece within 32-bit
+        // offsets (31 on the realignment path, whose word offsets are signed)
+        const auto sp = piece_span(pc);
+        const uint64_t lim = pc.realign ? kMaxChunkSpan / 2 : kMaxChunkSpan;
+        if (sp.first >= lim || sp.second >= lim) {  // (a single level is always monotone)
+            peel_top(p, pc, src_buf, fan_off, nfan, chunk_bytes);
+            return;
+        }
+    }
     uint64_t rows = 1;
     for (const auto &l : pc.outer) rows *= uint64_t(l.n);
     const uint64_t vpr = units_per_row(pc);
@@ -425,6 +464,113 @@ void split_emit(Plan &p, Piece pc, int32_t src_buf, int64_t fan_off, int64_t nfa
         sub.dst_off = pc.dst_off + uint64_t(i * top.ds);
         emit(p, sub, src_buf, fan_off, nfan, chunk_bytes);
     }
+}
+
+// Tile-transpose piece (see desc.h): A contiguous in the sender's buffer, B
+// in the receivers'; outer levels outermost first (any number: more than two
+// are peeled into separate pieces).
+struct TPiece {
+    uint64_t src_off, dst_off;
+    int64_t na, nb;            // extents of A and B (elements)
+    int64_t ss_b, ds_a;        // sender stride of B, receiver stride of A (bytes)
+    std::vector<Level> outer;  // outermost first
+};
+
+void emit_transpose(Plan &p, const TPiece &tp, int32_t src_buf, int64_t fan_off, int64_t nfan, int64_t chunk_bytes,
+                    std::vector<Desc> &out) {
+    if (p.too_many) return;
+    if (tp.outer.size() > 2) {
+        const Level top = tp.outer.front();
+        TPiece sub = tp;
+        sub.outer.erase(sub.outer.begin());
+        for (int64_t i = 0; i < top.n; ++i) {
+            sub.src_off = tp.src_off + uint64_t(i * top.ss);
+            sub.dst_off = tp.dst_off + uint64_t(i * top.ds);
+            emit_transpose(p, sub, src_buf, fan_off, nfan, chunk_bytes, out);
+        }
+        return;
+    }
+    const int64_t es = p.es;
+    const int64_t te = int64_t(tile_elems(uint32_t(es)));
+    {
+        // every tile is addressed from the piece's origin: the piece must lie
+        // within 32-bit offsets on both sides (else peel an outer level, or
+        // halve B in whole tiles)
+        uint64_t ss_ = uint64_t(tp.nb - 1) * uint64_t(tp.ss_b) + uint64_t(tp.na * es);
+        uint64_t sd_ = uint64_t(tp.na - 1) * uint64_t(tp.ds_a) + uint64_t(tp.nb * es);
+        for (const auto &l : tp.outer) {
+            ss_ += uint64_t(l.n - 1) * uint64_t(l.ss);
+            sd_ += uint64_t(l.n - 1) * uint64_t(l.ds);
+        }
+        if (ss_ >= kMaxChunkSpan || sd_ >= kMaxChunkSpan) {
+            if (!tp.outer.empty()) {
+                const Level top = tp.outer.front();
+                TPiece sub = tp;
+                sub.outer.erase(sub.outer.begin());
+                for (int64_t i = 0; i < top.n; ++i) {
+                    sub.src_off = tp.src_off + uint64_t(i * top.ss);
+                    sub.dst_off = tp.dst_off + uint64_t(i * top.ds);
+                    emit_transpose(p, sub, src_buf, fan_off, nfan, chunk_bytes, out);
+                }
+            } else {
+                const int64_t half = std::max<int64_t>(te, (tp.nb / 2) / te * te);
+                for (int64_t b0 = 0; b0 < tp.nb; b0 += half) {
+                    TPiece sub = tp;
+                    sub.nb = std::min(half, tp.nb - b0);
+                    sub.src_off = tp.src_off + uint64_t(b0 * tp.ss_b);
+                    sub.dst_off = tp.dst_off + uint64_t(b0 * es);
+                    emit_transpose(p, sub, src_buf, fan_off, nfan, chunk_bytes, out);
+                }
+            }
+            return;
+        }
+    }
+    const int nl = int(tp.outer.size());
+    const Level o1 = nl >= 1 ? tp.outer[size_t(nl - 1)] : Level{1, 0, 0};
+    const Level o2 = nl >= 2 ? tp.outer[0] : Level{1, 0, 0};
+    const uint64_t ntb = uint64_t((tp.nb + te - 1) / te), nta = uint64_t((tp.na + te - 1) / te);
+    const uint64_t tiles = ntb * nta * uint64_t(o1.n) * uint64_t(o2.n);
+    Desc d{};
+    bool ald = tp.src_off % 16 == 0 && tp.ss_b % 16 == 0 && o1.ss % 16 == 0 && o2.ss % 16 == 0;
+    bool ast = tp.dst_off % 16 == 0 && tp.ds_a % 16 == 0 && o1.ds % 16 == 0 && o2.ds % 16 == 0;
+    uint32_t log2es = 0;
+    while ((int64_t(1) << log2es) < es) ++log2es;
+    d.kind = uint8_t(log2es | (ald ? kTAlignLoad : 0u) | (ast ? kTAlignStore : 0u));
+    d.ss[0] = uint32_t(uint64_t(tp.ss_b));
+    d.ds[0] = uint32_t(uint64_t(tp.ds_a));
+    d.ss[1] = uint32_t(uint64_t(o1.ss));
+    d.ds[1] = uint32_t(uint64_t(o1.ds));
+    d.ss[2] = uint32_t(uint64_t(o2.ss));
+    d.ds[2] = uint32_t(uint64_t(o2.ds));
+    d.vpr = uint32_t(ntb);
+    d.n1 = uint32_t(nta);
+    d.n2 = uint32_t(o1.n);
+    const FastDiv f0 = make_fastdiv(d.vpr), f1 = make_fastdiv(d.n1), f2 = make_fastdiv(d.n2);
+    d.mul_vpr = f0.mul; d.sh_vpr = uint8_t(f0.shift);
+    d.mul_n1 = f1.mul;  d.sh_n1 = uint8_t(f1.shift);
+    d.mul_n2 = f2.mul;  d.sh_n2 = uint8_t(f2.shift);
+    d.run = uint32_t(tp.na);
+    d.batch = uint32_t(tp.nb);
+    d.src_buf = uint16_t(src_buf);
+    d.nfan = uint16_t(nfan);
+    d.fan_off = uint32_t(fan_off);
+    const uint64_t per = uint64_t(std::max<int64_t>(1, chunk_bytes / (te * te * es)));
+    if (p.descs.size() + out.size() + (tiles + per - 1) / per > kMaxDescs) {
+        p.too_many = true;
+        return;
+    }
+    d.src_base = tp.src_off;
+    d.dst_base = tp.dst_off;
+    d.src_rel0 = 0;
+    d.dst_rel0 = 0;
+    for (uint64_t t0 = 0; t0 < tiles;) {
+        const uint64_t t1 = std::min(tiles, t0 + per);
+        d.v0 = uint32_t(t0);
+        d.v1 = uint32_t(t1);
+        out.push_back(d);
+        t0 = t1;
+    }
+    p.align = std::max<int64_t>(p.align, (ald || ast) ? 16 : es);
 }
 
 int64_t auto_chunk_bytes(int64_t bytes_read) {
@@ -801,7 +947,12 @@ void lower(Plan &p) {
     p.gather_u_segs = 0;
     std::vector<Desc> gdescs, udescs;
     std::vector<char> handled(p.tasks.size(), 0);
-    if (!(p.flags & 0x100u) && !(p.flags & 0x60u)) {
+    bool permuted = false;
+    for (int k = 0; k < nd; ++k)
+        permuted = permuted || (!p.sperm.empty() && p.sperm[size_t(k)] != k) ||
+                   (!p.dperm.empty() && p.dperm[size_t(k)] != k);
+    std::vector<Desc> tdescs;
+    if (!(p.flags & 0x100u) && !(p.flags & 0x60u) && !permuted) {
         std::map<std::vector<int64_t>, std::vector<size_t>> groups;
         for (size_t i = 0; i < p.tasks.size(); ++i) {
             const UnitTask &t = p.tasks[i];
@@ -834,12 +985,16 @@ void lower(Plan &p) {
             ext_s[d] = p.src.bounds[d][js + 1] - p.src.bounds[d][js];
             ext_d[d] = p.dst.bounds[d][jd + 1] - p.dst.bounds[d][jd];
         }
+        // byte stride of each tensor dimension in the (possibly permuted)
+        // dense buffers: buffer dimension k is tensor dimension perm[k]
         int64_t a = es, b = es;
-        for (int d = nd - 1; d >= 0; --d) {
-            str_s[d] = a;
-            str_d[d] = b;
-            a *= ext_s[d];
-            b *= ext_d[d];
+        for (int k = nd - 1; k >= 0; --k) {
+            const int ds_ = p.sperm.empty() ? k : p.sperm[size_t(k)];
+            const int dd_ = p.dperm.empty() ? k : p.dperm[size_t(k)];
+            str_s[ds_] = a;
+            str_d[dd_] = b;
+            a *= ext_s[ds_];
+            b *= ext_d[dd_];
         }
         for (int d = 0; d < nd; ++d) {
             const int64_t js = p.src.dev_shard[int64_t(t.sender) * nd + d];
@@ -847,15 +1002,32 @@ void lower(Plan &p) {
             so += uint64_t((t.lo[d] - p.src.bounds[d][js]) * str_s[d]);
             dso += uint64_t((t.lo[d] - p.dst.bounds[d][jd]) * str_d[d]);
         }
-        // collapse: drop unit extents, merge dims contiguous on both sides
+        // collapse, in the receivers' dimension order: drop unit extents,
+        // merge dims contiguous on both sides
         std::vector<Level> g;  // innermost first while building
-        for (int d = nd - 1; d >= 0; --d) {
+        for (int k = nd - 1; k >= 0; --k) {
+            const int d = p.dperm.empty() ? k : p.dperm[size_t(k)];
             const int64_t n = t.hi[d] - t.lo[d];
             if (n == 1) continue;
             if (!g.empty() && str_s[d] == g.back().n * g.back().ss && str_d[d] == g.back().n * g.back().ds)
                 g.back().n *= n;
             else
                 g.push_back({n, str_s[d], str_d[d]});
+        }
+        // Contiguous along different dimensions on the two sides (a
+        // permuted layout): tiles transposed through LDS.
+        if (!g.empty() && g.front().ds == es && g.front().ss != es) {
+            size_t ia = 0;
+            for (size_t i = 1; i < g.size(); ++i)
+                if (g[i].ss == es) ia = i;
+            const int64_t te = int64_t(tile_elems(uint32_t(es)));
+            if (ia > 0 && te * g.front().ss < (int64_t(1) << 31) && te * g[ia].ds < (int64_t(1) << 31)) {
+                TPiece tp{so, dso, g[ia].n, g.front().n, g.front().ss, g[ia].ds, {}};
+                for (size_t i = g.size(); i-- > 1;)
+                    if (i != ia) tp.outer.push_back(g[i]);  // outermost first
+                emit_transpose(p, tp, t.sender, fan_off, nfan, chunk, tdescs);
+                continue;
+            }
         }
         int64_t run = es;
         if (!g.empty() && g.front().ss == es && g.front().ds == es) {
@@ -918,6 +1090,10 @@ void lower(Plan &p) {
     p.n_gather = gdescs.size();
     p.descs.insert(p.descs.begin() + std::ptrdiff_t(p.n_direct + p.n_gather), udescs.begin(), udescs.end());
     p.n_gather_u = udescs.size();
+    p.descs.insert(p.descs.begin() + std::ptrdiff_t(p.n_direct + p.n_gather + p.n_gather_u), tdescs.begin(),
+                   tdescs.end());
+    p.n_transpose = tdescs.size();
+    if (p.descs.size() > kMaxDescs) p.too_many = true;
     p.n_phase1 = p.n_direct;
     if (p.flags & 0x20u) {
         // Send/recv analogue (Section 3.1): the sender's slice is read once
@@ -992,9 +1168,11 @@ void lower(Plan &p) {
 
 void local_shape(const Plan &p, int side, int64_t dev, int64_t *out) {
     const Layout &L = side == 0 ? p.src : p.dst;
-    for (int d = 0; d < p.ndim; ++d) {
+    const std::vector<int> &perm = side == 0 ? p.sperm : p.dperm;
+    for (int k = 0; k < p.ndim; ++k) {
+        const int d = perm.empty() ? k : perm[size_t(k)];
         const int64_t j = L.dev_shard[dev * p.ndim + d];
-        out[d] = L.bounds[d][j + 1] - L.bounds[d][j];
+        out[k] = L.bounds[d][j + 1] - L.bounds[d][j];
     }
 }
 

@@ -67,6 +67,9 @@ struct Plan {
     unsigned flags = 0;
     Tuning tuning;
     Layout src, dst;
+    // Local layouts: dimension k of a device's buffer is tensor dimension
+    // perm[k] (identity unless the caller permuted a side).
+    std::vector<int> sperm, dperm;
     std::vector<UnitTask> tasks;
     std::vector<Desc> descs;
     std::vector<int32_t> fan;  // receiver lists, referenced by Desc::fan_off/nfan
@@ -77,6 +80,7 @@ struct Plan {
     size_t n_direct = 0;       // descs[0, n_direct): direct chunks
     size_t n_gather = 0;       // descs[n_direct, n_direct + n_gather): row-gather chunks;
     size_t n_gather_u = 0;     // then n_gather_u unaligned row-gather chunks;
+    size_t n_transpose = 0;    // then n_transpose tile-transpose chunks;
                                // the rest: realignment chunks
     std::vector<Seg> segs;     // row-gather segment entries
     int64_t gather_fanout = 0; // largest receiver count among row-gather chunks

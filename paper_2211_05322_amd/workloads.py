@@ -32,6 +32,8 @@ class Workload:
     src_spec: str
     dst_mesh: tuple
     dst_spec: str
+    src_perm: tuple = None  # buffer dimension order of each side (None: tensor order)
+    dst_perm: tuple = None
 
     @property
     def itemsize(self):
@@ -82,6 +84,18 @@ UNEVEN_WORKLOADS = {
 }
 
 
+# Reshards that also change the buffers' dimension order (the paper's specs
+# never do): the GPT activation stored [batch, hidden, seq] on the
+# destination, and the GPT-3-width one likewise with 4x replication.  Each
+# task is a tile transpose.
+TRANSPOSED_WORKLOADS = {
+    "transposed2": Workload("gpt_act_fp16_8x1024x4096_batch_to_seq_hidden_major", (8, 1024, 4096), "float16",
+                            "normal", (2, 4), "S^0 R S^1", (2, 4), "R S^0 S^1", None, (0, 2, 1)),
+    "transposed5": Workload("gpt3_act_fp16_8x2048x12288_hidden32_to_seq8x4rep_hidden_major", (8, 2048, 12288),
+                            "float16", "normal", (4, 8), "R R S^{01}", (4, 8), "R S^1 R", None, (0, 2, 1)),
+}
+
+
 # The multi-to-multi microbenchmark of the paper's Table 3: tensor
 # (1024, 1024, 512), (case, send spec, recv spec, send mesh, recv mesh); a
 # mesh row is one node.  Table 3 prints case 1's send mesh as "(2.4)" and case
@@ -111,12 +125,15 @@ def fanout_workload(receivers, nbytes=1 << 30):
 
 
 def workload_by_name(key):
-    """WORKLOADS id (1..5 or "1".."5"), an UNEVEN_WORKLOADS key, or "fanoutR" (R receivers, 1 GiB)."""
+    """WORKLOADS id (1..5 or "1".."5"), an UNEVEN_WORKLOADS or TRANSPOSED_WORKLOADS key, or "fanoutR"
+    (R receivers, 1 GiB)."""
     key = str(key)
     if key.startswith("fanout"):
         return fanout_workload(int(key[len("fanout"):]))
     if key in UNEVEN_WORKLOADS:
         return UNEVEN_WORKLOADS[key]
+    if key in TRANSPOSED_WORKLOADS:
+        return TRANSPOSED_WORKLOADS[key]
     return WORKLOADS[int(key)]
 
 

@@ -10,6 +10,7 @@
 #include <cstdlib>
 #include <cstring>
 #include <string>
+#include <utility>
 #include <vector>
 
 #include "reshard.h"
@@ -73,9 +74,18 @@ int main(int argc, char **argv) {
             tn.chunk_bytes = rnd(3) == 0 ? 0 : int64_t(16 + rnd(3000));
             tn.block_threads = 64 << rnd(5);
             tn.gather_band = int32_t(rnd(4));
+            // permuted local layouts (not with the comparison strategies)
+            int32_t sperm[4], dperm[4];
+            for (int d = 0; d < nd; ++d) sperm[d] = dperm[d] = d;
+            const bool permute = rnd(2) == 0 && !(flags & (RESHARD_STRATEGY_SENDRECV | RESHARD_STRATEGY_ALLGATHER));
+            if (permute)
+                for (int d = nd - 1; d > 0; --d) {
+                    std::swap(sperm[d], sperm[rnd(uint32_t(d + 1))]);
+                    std::swap(dperm[d], dperm[rnd(uint32_t(d + 1))]);
+                }
             reshard_plan_t *p = nullptr;
-            if (reshard_plan_ex(nd, shape, dts[di], smn, sm, ss.c_str(), dmn, dm, ds.c_str(), flags, &tn, &p) !=
-                RESHARD_OK) {
+            if (reshard_plan_permuted(nd, shape, dts[di], smn, sm, ss.c_str(), sperm, dmn, dm, ds.c_str(), dperm,
+                                      flags, &tn, &p) != RESHARD_OK) {
                 fprintf(stderr, "plan failed: %s\n", reshard_last_error());
                 return 1;
             }

@@ -138,7 +138,7 @@ def run_host(p, src_arrays, dst_shapes, np_dtype):
     dp = [r.ctypes.data + GUARD if r.size > 2 * GUARD else None for r in dsts]
     for q in sp + dp:
         assert q is None or q % 16 == 0
-    B.load().reshard_debug_execute_host(p.handle, B._ptrs(sp), B._ptrs(dp))
+    B._check(B.load().reshard_debug_execute_host(p.handle, B._ptrs(sp), B._ptrs(dp)))
     outs = []
     for r, s in zip(dsts, dst_shapes):
         assert (r[:GUARD] == 0x5A).all() and (r[r.size - GUARD:] == 0x5A).all(), "write outside buffer"
