@@ -343,14 +343,15 @@ reshard_status_t reshard_debug_execute_host(const reshard_plan_t *plan, void *co
                 // tile-transpose chunk: the kernel's tile arithmetic and
                 // swizzled LDS tile, every access bounds-checked
                 const uint32_t es = uint32_t(p->es), te = rs::tile_elems(es), vpe = 16u / es;
+                const uint32_t tr = rs::tile_rows(es, d.kind), slots = tr * es / 16u;  // per column
                 const bool ald = (d.kind & rs::kTAlignLoad) != 0, ast = (d.kind & rs::kTAlignStore) != 0;
                 if ((1u << (d.kind & 0xFu)) != es) return fail(RESHARD_EINVAL, "internal: transpose element size");
                 const uint64_t sbytes = uint64_t(p->src_local_numel[d.src_buf] * p->es);
-                lds.assign(te * rs::kTileBytes, 0);
+                lds.assign(tr * rs::kTileBytes, 0);
                 for (uint32_t t = d.v0; t < d.v1; ++t) {
                     const rs::TileAt at = rs::tile_offsets(d, t, es);
-                    const uint32_t na = std::min(te, d.run - at.ta * te), nb = std::min(te, d.batch - at.tb * te);
-                    for (uint32_t i = 0; i < te * 8u; ++i) {  // load phase
+                    const uint32_t na = std::min(te, d.run - at.ta * te), nb = std::min(tr, d.batch - at.tb * tr);
+                    for (uint32_t i = 0; i < tr * 8u; ++i) {  // load phase
                         const uint32_t r = i >> 3, c = i & 7u;
                         if (r >= nb) continue;
                         const uint32_t a0 = c * vpe;
@@ -371,8 +372,8 @@ reshard_status_t reshard_debug_execute_host(const reshard_plan_t *plan, void *co
                         if (o + 16 > lds.size()) return fail(RESHARD_EINVAL, "internal: transpose LDS write out of range");
                         std::memcpy(lds.data() + o, x, 16);
                     }
-                    for (uint32_t i = 0; i < te * 8u; ++i) {  // store phase
-                        const uint32_t a = i >> 3, j = i & 7u;
+                    for (uint32_t i = 0; i < te * slots; ++i) {  // store phase
+                        const uint32_t a = i / slots, j = i % slots;
                         if (a >= na) continue;
                         const uint32_t b0 = j * vpe;
                         const uint32_t nv = b0 < nb ? std::min(vpe, nb - b0) : 0u;

@@ -140,7 +140,8 @@ constexpr uint32_t kMaxSegs = 256;  // segment entries one gather chunk may stag
 // kTileBytes contiguous source bytes, its columns (one per A index)
 // kTileBytes contiguous destination bytes.  A chunk is a range of tiles of a
 // piece (tile t: tb = t mod ntb fastest, then ta, then the outer levels o1,
-// o2).  Fields: kind = log2 es | kTAlignLoad | kTAlignStore; ss[0] = sender
+// o2).  Fields: kind = log2 es | kTAlignLoad | kTAlignStore | (log2 of the
+// width factor along B) << 6; ss[0] = sender
 // stride of B, ds[0] = receiver stride of A; ss[1], ds[1] and ss[2], ds[2]
 // the outer levels o1 (inner) and o2; vpr = ntb, n1 = nta, n2 = extent of o1
 // (with their fast divisions); run = extent of A, batch = extent of B
@@ -152,6 +153,12 @@ constexpr uint32_t kTileBytes = 128;
 constexpr uint32_t kTAlignLoad = 0x10u;
 constexpr uint32_t kTAlignStore = 0x20u;
 constexpr uint32_t tile_elems(uint32_t es) { return kTileBytes / es; }
+// A tile spans 1, 2 or 4 x kTileBytes along B (kind bits 6-7 hold log2 of
+// that factor): wide enough to write whole destination rows of up to 512
+// bytes, so each tile fills every cache line of the rows it writes.  Its
+// LDS image is (B extent) rows of kTileBytes.
+constexpr uint32_t tile_wide_log2(uint32_t kind) { return (kind >> 6) & 3u; }
+constexpr uint32_t tile_rows(uint32_t es, uint32_t kind) { return tile_elems(es) << tile_wide_log2(kind); }
 
 // Relative offsets (sender, receiver) of tile t's origin from the chunk's
 // first tile (mod 2^32), and the tile's (ta, tb) indices.
@@ -166,9 +173,9 @@ constexpr TileAt tile_offsets(const Desc &d, uint32_t t, uint32_t es) {
     const uint32_t ta = r - o * d.n1;
     const uint32_t o2 = fastdiv(o, d.mul_n2, d.sh_n2);
     const uint32_t o1 = o - o2 * d.n2;
-    const uint32_t te = tile_elems(es);
-    const uint32_t s = tb * te * d.ss[0] + ta * kTileBytes + o1 * d.ss[1] + o2 * d.ss[2];
-    const uint32_t u = ta * te * d.ds[0] + tb * kTileBytes + o1 * d.ds[1] + o2 * d.ds[2];
+    const uint32_t te = tile_elems(es), tr = tile_rows(es, d.kind);
+    const uint32_t s = tb * tr * d.ss[0] + ta * kTileBytes + o1 * d.ss[1] + o2 * d.ss[2];
+    const uint32_t u = ta * te * d.ds[0] + tb * (tr * es) + o1 * d.ds[1] + o2 * d.ds[2];
     return TileAt{s - d.src_rel0, u - d.dst_rel0, ta, tb};
 }
 

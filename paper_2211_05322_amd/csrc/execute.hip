@@ -878,16 +878,18 @@ __device__ __forceinline__ void store_elems(RS_GLOBAL unsigned char *q, u32x4 y,
 template <int ES, int NPTR>
 __device__ __forceinline__ void run_transpose(const Desc &d, const RS_CONST KArgs<NPTR> *a) {
     constexpr uint32_t T = kTileBytes / ES, V = 16u / ES;
+    const uint32_t TR = tile_rows(ES, d.kind), SL = TR * ES / 16u;  // tile rows; 16-byte slots per column
     unsigned char *lds = rs_lds;
     const RS_GLOBAL unsigned char *src = (const RS_GLOBAL unsigned char *)a->ptr[d.src_buf] + d.src_base;
     const RS_CONST int32_t *fan = (const RS_CONST int32_t *)(a->fan + d.fan_off);
     const bool ald = (d.kind & kTAlignLoad) != 0, ast = (d.kind & kTAlignStore) != 0;
     const uint32_t nthr = blockDim.x, tid = threadIdx.x;
+    const uint32_t wl2 = tile_wide_log2(d.kind);
     for (uint32_t t = d.v0; t < d.v1; ++t) {
         const TileAt at = tile_offsets(d, t, ES);
         const uint32_t na = d.run - at.ta * T < T ? d.run - at.ta * T : T;
-        const uint32_t nb = d.batch - at.tb * T < T ? d.batch - at.tb * T : T;
-        for (uint32_t i = tid; i < T * 8u; i += nthr) {
+        const uint32_t nb = d.batch - at.tb * TR < TR ? d.batch - at.tb * TR : TR;
+        for (uint32_t i = tid; i < TR * 8u; i += nthr) {
             const uint32_t r = i >> 3, c = i & 7u;
             if (r >= nb) continue;
             const uint32_t a0 = c * V;
@@ -899,8 +901,8 @@ __device__ __forceinline__ void run_transpose(const Desc &d, const RS_CONST KArg
             tile_put<ES>(lds, tile_lds(r, c, 0, ES), x);
         }
         __syncthreads();
-        for (uint32_t i = tid; i < T * 8u; i += nthr) {
-            const uint32_t aa = i >> 3, j = i & 7u;
+        for (uint32_t i = tid; i < T * SL; i += nthr) {
+            const uint32_t aa = i >> (3u + wl2), j = i & (SL - 1u);
             if (aa >= na) continue;
             const uint32_t b0 = j * V;
             const uint32_t nv = b0 < nb ? (nb - b0 < V ? nb - b0 : V) : 0u;
@@ -1117,11 +1119,11 @@ reshard_status_t launch(const Plan &p, const Desc *descs, const int32_t *fan, co
         if (st != RESHARD_OK) return st;
     }
     if (n_transpose) {
-        // the tile (kTileBytes rows of kTileBytes / es elements) in LDS;
+        // the widest tile of the plan (rows of kTileBytes) in LDS;
         // no residency cap
         a.descs = descs + n_direct + n_gather + n_gather_u;
         const uint32_t tblock = block < 256u ? block : 256u;
-        const uint32_t lds = (kTileBytes / uint32_t(p.es)) * kTileBytes;
+        const uint32_t lds = p.transpose_rows * kTileBytes;
         const reshard_status_t st =
             launch_one(reshard_transpose_kernel<NPTR>, a, n_transpose, remap, tblock, lds, stream);
         if (st != RESHARD_OK) return st;

@@ -466,6 +466,10 @@ void split_emit(Plan &p, Piece pc, int32_t src_buf, int64_t fan_off, int64_t nfa
     }
 }
 
+#ifndef RS_TMAXW_LOG2
+#define RS_TMAXW_LOG2 2u  // widest tile along B: 4 x 128 bytes
+#endif
+
 // Tile-transpose piece (see desc.h): A contiguous in the sender's buffer, B
 // in the receivers'; outer levels outermost first (any number: more than two
 // are peeled into separate pieces).
@@ -513,7 +517,7 @@ void emit_transpose(Plan &p, const TPiece &tp, int32_t src_buf, int64_t fan_off,
                     emit_transpose(p, sub, src_buf, fan_off, nfan, chunk_bytes, out);
                 }
             } else {
-                const int64_t half = std::max<int64_t>(te, (tp.nb / 2) / te * te);
+                const int64_t half = std::max<int64_t>(4 * te, (tp.nb / 2) / (4 * te) * (4 * te));
                 for (int64_t b0 = 0; b0 < tp.nb; b0 += half) {
                     TPiece sub = tp;
                     sub.nb = std::min(half, tp.nb - b0);
@@ -528,14 +532,19 @@ void emit_transpose(Plan &p, const TPiece &tp, int32_t src_buf, int64_t fan_off,
     const int nl = int(tp.outer.size());
     const Level o1 = nl >= 1 ? tp.outer[size_t(nl - 1)] : Level{1, 0, 0};
     const Level o2 = nl >= 2 ? tp.outer[0] : Level{1, 0, 0};
-    const uint64_t ntb = uint64_t((tp.nb + te - 1) / te), nta = uint64_t((tp.na + te - 1) / te);
+    // tile width along B: up to 4 x 128 bytes, enough for the B extent, with
+    // at most 256 tile rows (32 KiB of LDS)
+    uint32_t wide = 0;
+    while (wide < RS_TMAXW_LOG2 && (te << wide) * es < tp.nb * es && (te << (wide + 1)) <= 256) ++wide;
+    const int64_t tr = te << wide;
+    const uint64_t ntb = uint64_t((tp.nb + tr - 1) / tr), nta = uint64_t((tp.na + te - 1) / te);
     const uint64_t tiles = ntb * nta * uint64_t(o1.n) * uint64_t(o2.n);
     Desc d{};
     bool ald = tp.src_off % 16 == 0 && tp.ss_b % 16 == 0 && o1.ss % 16 == 0 && o2.ss % 16 == 0;
     bool ast = tp.dst_off % 16 == 0 && tp.ds_a % 16 == 0 && o1.ds % 16 == 0 && o2.ds % 16 == 0;
     uint32_t log2es = 0;
     while ((int64_t(1) << log2es) < es) ++log2es;
-    d.kind = uint8_t(log2es | (ald ? kTAlignLoad : 0u) | (ast ? kTAlignStore : 0u));
+    d.kind = uint8_t(log2es | (ald ? kTAlignLoad : 0u) | (ast ? kTAlignStore : 0u) | (wide << 6));
     d.ss[0] = uint32_t(uint64_t(tp.ss_b));
     d.ds[0] = uint32_t(uint64_t(tp.ds_a));
     d.ss[1] = uint32_t(uint64_t(o1.ss));
@@ -554,7 +563,7 @@ void emit_transpose(Plan &p, const TPiece &tp, int32_t src_buf, int64_t fan_off,
     d.src_buf = uint16_t(src_buf);
     d.nfan = uint16_t(nfan);
     d.fan_off = uint32_t(fan_off);
-    const uint64_t per = uint64_t(std::max<int64_t>(1, chunk_bytes / (te * te * es)));
+    const uint64_t per = uint64_t(std::max<int64_t>(1, chunk_bytes / (te * tr * es)));
     if (p.descs.size() + out.size() + (tiles + per - 1) / per > kMaxDescs) {
         p.too_many = true;
         return;
@@ -571,6 +580,7 @@ void emit_transpose(Plan &p, const TPiece &tp, int32_t src_buf, int64_t fan_off,
         t0 = t1;
     }
     p.align = std::max<int64_t>(p.align, (ald || ast) ? 16 : es);
+    p.transpose_rows = std::max(p.transpose_rows, uint32_t(tr));
 }
 
 int64_t auto_chunk_bytes(int64_t bytes_read) {
@@ -933,6 +943,7 @@ void lower(Plan &p) {
     p.fan.assign(p.dst.shard_devs.begin(), p.dst.shard_devs.end());
     p.align = 1;
     p.lds_bytes = 0;
+    p.transpose_rows = 0;
     p.too_many = false;
     p.max_fanout = 0;
     p.bytes_read = 0;

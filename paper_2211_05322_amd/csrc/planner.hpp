@@ -81,6 +81,7 @@ struct Plan {
     size_t n_gather = 0;       // descs[n_direct, n_direct + n_gather): row-gather chunks;
     size_t n_gather_u = 0;     // then n_gather_u unaligned row-gather chunks;
     size_t n_transpose = 0;    // then n_transpose tile-transpose chunks;
+    uint32_t transpose_rows = 0;  // rows of the widest transpose tile (LDS: rows x 128 bytes)
                                // the rest: realignment chunks
     std::vector<Seg> segs;     // row-gather segment entries
     int64_t gather_fanout = 0; // largest receiver count among row-gather chunks
