@@ -434,20 +434,25 @@ reshard_status_t reshard_debug_execute_host(const reshard_plan_t *plan, void *co
                     uint32_t row = d.ss[0] + dr, col = t - dr * rb;
                     uint32_t g = find_segment(col);
                     const uint32_t send = g + 1 < ns ? sg[g + 1].col : rb;
-                    const uint32_t e1 = lo + std::min(hi - lo, send - col);
-                    if (!piece(row, g, col, e1 - lo, out + (lo - c0)))
-                        return fail(RESHARD_EINVAL, "internal: unaligned gather piece outside its segment or shard");
-                    if (e1 < hi) {
-                        if (send == rb) {
+                    // pieces in turn: the rest of this segment (or row), then
+                    // the next segments (any number when segments are short)
+                    uint32_t at = lo, send_g = send;
+                    for (;;) {
+                        const uint32_t e = at + std::min(hi - at, send_g - col);
+                        if (!piece(row, g, col, e - at, out + (at - c0)))
+                            return fail(RESHARD_EINVAL, "internal: unaligned gather piece outside its segment or shard");
+                        if (e >= hi) break;
+                        if (send_g == rb) {
                             ++row;
                             col = 0;
                             g = 0;
                         } else {
-                            col = send;
+                            col = send_g;
                             ++g;
                         }
-                        if (!piece(row, g, col, hi - e1, out + (e1 - c0)))
-                            return fail(RESHARD_EINVAL, "internal: unaligned gather piece outside its segment or shard");
+                        if (g >= ns) return fail(RESHARD_EINVAL, "internal: unaligned gather segment index out of range");
+                        send_g = g + 1 < ns ? sg[g + 1].col : rb;
+                        at = e;
                     }
                     for (uint32_t r = 0; r < d.nfan; ++r) {
                         const int32_t dev = p->fan[d.fan_off + r];

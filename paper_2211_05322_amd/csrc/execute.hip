@@ -627,6 +627,8 @@ struct USlot {
     u32x4 a0, a1, b0, b1;   // aligned source words of the two pieces
     uint32_t lo, hi, e1;    // slot bytes [lo, hi) in chunk coordinates; piece 2 starts at e1
     uint32_t sha, shb;      // byte offsets of the pieces in their first words
+    uint32_t e2;            // piece 2 ends at e2: hi, unless a segment shorter than the rest follows
+    uint32_t row, col, g;   // where the bytes from e2 on start (segments shorter than 16 bytes)
 };
 
 template <int L>
@@ -638,8 +640,12 @@ __device__ __forceinline__ void uslot_load(const Desc &d, const uint64_t *sp, co
     s.lo = c0 > d.ss[2] ? c0 : d.ss[2];
     s.hi = c0 + 16u < d.src_rel0 ? c0 + 16u : d.src_rel0;
     s.e1 = s.hi;
+    s.e2 = s.hi;
     s.sha = 0;
     s.shb = 0;
+    s.row = 0;
+    s.col = 0;
+    s.g = 0;
     if (s.lo >= s.hi) return;
     const uint32_t rb = d.vpr, ns = d.pad[1];
     const uint32_t t = s.lo + d.ss[1];  // >= 0: the region starts at ss[2] = -cofs0 in the first chunk
@@ -661,11 +667,64 @@ __device__ __forceinline__ void uslot_load(const Desc &d, const uint64_t *sp, co
             col = send;
             ++g;
         }
+        const uint32_t send2 = g + 1 < ns ? scol[g + 1] : rb;
+        s.e2 = s.e1 + ((s.hi - s.e1) < (send2 - col) ? (s.hi - s.e1) : (send2 - col));
         q = segment_addr<L>(d, sp, sst, scol, g, row, col);
         s.shb = uint32_t(q) & 15u;
         s.b0 = load_vec((const RS_GLOBAL u32x4 *)(q & ~uint64_t(15)));
-        if (s.shb + (s.hi - s.e1) > 16u) s.b1 = load_vec((const RS_GLOBAL u32x4 *)((q & ~uint64_t(15)) + 16u));
+        if (s.shb + (s.e2 - s.e1) > 16u) s.b1 = load_vec((const RS_GLOBAL u32x4 *)((q & ~uint64_t(15)) + 16u));
+        if (s.e2 < s.hi) {  // a short segment: the bytes from e2 on come from the pieces after it
+            if (send2 == rb) {
+                ++row;
+                col = 0;
+                g = 0;
+            } else {
+                col = send2;
+                ++g;
+            }
+            s.row = row;
+            s.col = col;
+            s.g = g;
+        }
     }
+}
+
+// Slot bytes [e2, hi) of a slot cut by segments shorter than 16 bytes (the
+// rare third and later pieces): one byte load each, the segment walk
+// continued from (row, col, g).
+template <int L>
+__device__ __forceinline__ u32x4 uslot_rest(const Desc &d, const uint64_t *sp, const uint32_t *sst,
+                                            const uint32_t *scol, const USlot &s, uint32_t c0, u32x4 out) {
+    const uint32_t rb = d.vpr, ns = d.pad[1];
+    uint32_t row = s.row, col = s.col, g = s.g;
+    uint32_t send = g + 1 < ns ? scol[g + 1] : rb;
+    uint64_t q = segment_addr<L>(d, sp, sst, scol, g, row, col);
+    uint32_t w0 = out.x, w1 = out.y, w2 = out.z, w3 = out.w;
+    for (uint32_t k = s.e2 - c0; k < s.hi - c0; ++k) {
+        if (col == send) {
+            if (send == rb) {
+                ++row;
+                col = 0;
+                g = 0;
+            } else {
+                ++g;
+            }
+            send = g + 1 < ns ? scol[g + 1] : rb;
+            q = segment_addr<L>(d, sp, sst, scol, g, row, col);
+        }
+        const uint32_t b = *(const RS_GLOBAL unsigned char *)q;
+        const uint32_t sh = 8u * (k & 3u), m = ~(0xFFu << sh);
+        const uint32_t wi = k >> 2;
+        w0 = wi == 0 ? (w0 & m) | (b << sh) : w0;
+        w1 = wi == 1 ? (w1 & m) | (b << sh) : w1;
+        w2 = wi == 2 ? (w2 & m) | (b << sh) : w2;
+        w3 = wi == 3 ? (w3 & m) | (b << sh) : w3;
+        ++col;
+        ++q;
+    }
+    u32x4 r;
+    r.x = w0; r.y = w1; r.z = w2; r.w = w3;
+    return r;
 }
 
 // v's bytes moved up by o (0..15): result byte j = v[j - o], zero below o.
@@ -718,8 +777,10 @@ __device__ __forceinline__ void run_gather_u(const Desc &d, const RS_CONST KArgs
         USlot s0, s1;
         uslot_load<L>(d, sp, sst, scol, c0, s0);
         if (has1) uslot_load<L>(d, sp, sst, scol, c1, s1);
-        const u32x4 o0 = uslot_compose(s0, c0);
-        const u32x4 o1 = has1 ? uslot_compose(s1, c1) : o0;
+        u32x4 o0 = uslot_compose(s0, c0);
+        u32x4 o1 = has1 ? uslot_compose(s1, c1) : o0;
+        if (s0.e2 < s0.hi) o0 = uslot_rest<L>(d, sp, sst, scol, s0, c0, o0);
+        if (has1 && s1.e2 < s1.hi) o1 = uslot_rest<L>(d, sp, sst, scol, s1, c1, o1);
         if constexpr (RF >= 1 && RF <= 4) {
 #pragma unroll
             for (uint32_t r = 0; r < nr; ++r)

@@ -753,6 +753,10 @@ bool lower_gather_group(Plan &p, const std::vector<size_t> &group, int64_t chunk
     return true;
 }
 
+#ifndef RS_UG_MIN_RUN
+#define RS_UG_MIN_RUN 2048u
+#endif
+
 // Unaligned row gather of one group (see desc.h): segments of any widths of
 // at least 16 bytes tiling the destination row (one segment per row too,
 // when its rows are in different 16-byte phases on the two sides),
@@ -775,11 +779,12 @@ bool lower_gather_unaligned(Plan &p, const std::vector<size_t> &group, int64_t c
         ext_d[d] = p.dst.bounds[d][jd + 1] - dlo[d];
     }
     for (int d = nd - 1; d >= 0; --d) str_d[d] = d == nd - 1 ? es : str_d[d + 1] * ext_d[d + 1];
-    // the segments tile the destination row, each at least 16 bytes
+    // the segments tile the destination row (segments shorter than 16 bytes
+    // make some slots hold more than two pieces: the kernel's rare path)
     int64_t at = dlo[nd - 1];
     for (size_t k : g) {
         const UnitTask &t = p.tasks[k];
-        if (t.lo[nd - 1] != at || (t.hi[nd - 1] - t.lo[nd - 1]) * es < 16) return false;
+        if (t.lo[nd - 1] != at) return false;
         at = t.hi[nd - 1];
     }
     if (at != dlo[nd - 1] + ext_d[nd - 1]) return false;
@@ -880,9 +885,10 @@ bool lower_gather_unaligned(Plan &p, const std::vector<size_t> &group, int64_t c
     d.pad[0] = uint32_t(p.segs.size());
     d.pad[1] = uint32_t(ns);
     const uint64_t cv = uint64_t(std::max<int64_t>(16, chunk_bytes / 16)) / 16 * 16;
-    // runs shorter than a chunk stay with the per-task lowering: each run is
-    // chunked on its own, so short runs would make short chunks
-    if (brk >= 0 && (run_bytes < 16 * cv || rows / run_rows > kMaxDescs / 4)) return false;
+    // each run is chunked on its own: runs shorter than RS_UG_MIN_RUN bytes
+    // (which would make very short chunks) stay with the per-task lowering
+    if (brk >= 0 && (run_bytes < std::min<uint64_t>(16 * cv, RS_UG_MIN_RUN) || rows / run_rows > kMaxDescs / 4))
+        return false;
     // run starts in the receivers' buffers, C order over dimensions 0..brk
     std::vector<uint64_t> run_d0(1, d0);
     for (int d = 0; d <= brk; ++d) {

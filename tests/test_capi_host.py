@@ -283,11 +283,16 @@ def test_host_unaligned_gather_in_runs(case, chunk):
     host_case(*case, chunk_bytes=chunk)
 
 
-def test_short_runs_keep_the_realignment_path():
-    # runs of 21 or 20 rows x 154 bytes (about 3 KiB) are shorter than the
-    # automatic chunk of this small tensor (4 KiB)
+def test_short_runs():
+    # runs of 21 or 20 rows x 154 bytes (about 3 KiB, shorter than the
+    # automatic 4 KiB chunk) take the unaligned row gather, one short chunk
+    # per run; runs of 6 or 5 rows (under 1 KiB) keep the realignment path
     p = plan_of((4, 41, 77), "float16", (2, 2), "R S^0 S^1", (2,), "S^0 R R")
+    assert B.reshard_plan_unaligned_gather_chunks(p) > 0 and B.reshard_plan_realign_chunks(p) == 0
+    host_case((4, 41, 77), "float16", (2, 2), "R S^0 S^1", (2,), "S^0 R R")
+    p = plan_of((4, 11, 77), "float16", (2, 2), "R S^0 S^1", (2,), "S^0 R R")
     assert B.reshard_plan_unaligned_gather_chunks(p) == 0 and B.reshard_plan_realign_chunks(p) > 0
+    host_case((4, 11, 77), "float16", (2, 2), "R S^0 S^1", (2,), "S^0 R R")
 
 
 def test_aligned_workloads_do_not_realign():
@@ -486,15 +491,31 @@ def test_host_unaligned_gather(case, chunk):
 
 
 def test_unaligned_gather_declines():
-    # segments under 16 bytes, destination rows that are not contiguous, or
-    # one sender per row with both sides in the same 16-byte phase:
-    # per-task chunks instead
-    for case in (((4, 8, 40), "float16", (8,), "RRS^0", (2,), "S^0RR"),
-                 ((6, 10, 300), "float16", (2, 3), "RS^0S^1", (2,), "RRS^0"),
+    # destination rows that are not contiguous, or one sender per row with
+    # both sides in the same 16-byte phase: per-task chunks instead
+    for case in (((6, 10, 300), "float16", (2, 3), "RS^0S^1", (2,), "RRS^0"),
                  ((8, 64, 1024), "float16", (1,), "RRR", (4,), "RRS^0")):
         p = plan_of(*case)
         assert B.reshard_plan_unaligned_gather_chunks(p) == 0
         host_case(*case)
+
+
+SHORT_SEGMENT_CASES = [
+    # segments under 16 bytes: slots of three or more pieces
+    ((4, 8, 40), "float16", (8,), "RRS^0", (2,), "S^0RR"),              # 10-byte segments
+    ((3, 16, 60), "uint8", (1, 8), "RRS^1", (2,), "RRR"),              # 8/7-byte segments, fan-out 2
+    ((2, 12, 27), "float32", (1, 3, 3), "RRS^{12}", (1,), "RRR"),      # 12-byte segments
+    ((2, 64, 12300), "float16", (4, 8), "RRS^{01}", (4, 8), "S^0RS^1"),  # a 4-byte segment at most row starts
+    ((5, 40, 33), "uint8", (1, 11), "RRS^1", (3,), "S^0RR"),           # 3-byte segments
+]
+
+
+@pytest.mark.parametrize("case", SHORT_SEGMENT_CASES)
+@pytest.mark.parametrize("chunk", [0, 64, 1000])
+def test_host_unaligned_gather_short_segments(case, chunk):
+    p = plan_of(*case, chunk_bytes=chunk)
+    assert B.reshard_plan_unaligned_gather_chunks(p) > 0 and B.reshard_plan_realign_chunks(p) == 0
+    host_case(*case, chunk_bytes=chunk)
 
 
 def test_gather_used_by_column_split_workloads():

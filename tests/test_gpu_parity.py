@@ -337,7 +337,19 @@ def test_gather_path(case):
 
 # ------------------------------------------------- unaligned row gather
 
-from tests.test_capi_host import UNALIGNED_GATHER_CASES  # noqa: E402
+from tests.test_capi_host import SHORT_SEGMENT_CASES, UNALIGNED_GATHER_CASES  # noqa: E402
+
+
+@pytest.mark.parametrize("case", SHORT_SEGMENT_CASES + [((4, 41, 77), "float16", (2, 2), "R S^0 S^1", (2,), "S^0 R R")])
+def test_unaligned_gather_short_segments_and_runs(case):
+    # segments under 16 bytes (slots of three or more pieces) and runs
+    # shorter than a chunk, on the unaligned row gather
+    shape, dt, sm, ss, dm, ds = case
+    _say(f"short segments / runs {case}")
+    assert B.reshard_plan_unaligned_gather_chunks(B.reshard_plan(shape, dt, sm, ss, dm, ds)) > 0
+    for kw in ({}, {"chunk_bytes": 64, "block_threads": 64}, {"chunk_bytes": 1000}, {"max_wgs_per_cu": -1}):
+        got, want = run_gpu(shape, dt, sm, ss, dm, ds, rand_bits(shape, dt, 15), **kw)
+        assert_same(got, want)
 
 
 @pytest.mark.parametrize("case", UNALIGNED_GATHER_CASES)
