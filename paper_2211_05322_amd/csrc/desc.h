@@ -122,12 +122,28 @@ static_assert(sizeof(Desc) == 112, "descriptor layout is shared by host and devi
 // pad[0], pad[1] the segment entries.  Each entry's `col` is its first byte
 // within the row; its src_base is the source offset of the group's first row
 // at that column (any byte alignment).
+//
+// Unit gather (kind | kUnitGather, in the unaligned row-gather section, for
+// one receiver and segments of at least 16 bytes): lanes take 16-byte units
+// of each segment's row rather than slots of the destination -- unit k of a
+// segment of width w covers bytes [min(16k, w - 16), +16), so the last unit
+// overlaps the one before it and rewrites the same bytes -- each one
+// unaligned 16-byte load and one unaligned 16-byte store, with no shifts or
+// merges.  Fields: v0, v1 = units [v0, v1) of the region (unit v is unit
+// v mod vpr of region row v / vpr); vpr = units per row with mul_vpr /
+// sh_vpr; n1, n2 and their multipliers = the source levels; ss[0] = the
+// region's first row in group numbering, ss[1] = the chunk's first region
+// row; dst_base = that row's byte offset in the receivers' buffers; run =
+// row bytes; batch / pad[2] = fast division by the nominal units per
+// segment (a first guess); pad[0], pad[1] the segment entries, whose `pad`
+// holds the segment's first unit within the row.
+constexpr uint32_t kUnitGather = 0x08u;
 struct Seg {
     uint64_t src_base;
     uint32_t ss[3];
     uint32_t buf;
     uint32_t col;  // unaligned gather: first byte of the segment within the row
-    uint32_t pad;
+    uint32_t pad;  // unit gather: first unit of the segment within the row
 };
 static_assert(sizeof(Seg) == 32, "segment entries are shared by host and device");
 constexpr uint32_t kMaxSegs = 256;  // segment entries one gather chunk may stage

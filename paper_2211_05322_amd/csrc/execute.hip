@@ -572,7 +572,7 @@ __global__ __launch_bounds__(1024) void reshard_gather_kernel(KArgs<NPTR> args) 
 // byte of its piece, so no load leaves the 4 KiB page of a byte it needs.
 // LDS: 64-bit source pointers at 0, three strides per segment at
 // 8 * kMaxSegs, segment starts (bytes within the row) at 20 * kMaxSegs.
-constexpr uint32_t kGatherULds = 24u * kMaxSegs;
+constexpr uint32_t kGatherULds = 28u * kMaxSegs;  // + first units (unit gather) at 24 * kMaxSegs
 
 // Chunk order of the unaligned row gather: the dispatcher hands workgroups to
 // the 8 XCDs in turn, so blocks b, b + 8, ..., b + 8 (kUGroup - 1) share an
@@ -600,6 +600,7 @@ __device__ __forceinline__ void stage_segments_u(const Desc &d, const RS_CONST K
         sst[3 * g + 1] = segs[g].ss[1];
         sst[3 * g + 2] = segs[g].ss[2];
         scol[g] = segs[g].col;
+        reinterpret_cast<uint32_t *>(rs_lds + 24u * kMaxSegs)[g] = segs[g].pad;
     }
 }
 
@@ -810,8 +811,67 @@ __device__ __forceinline__ void run_gather_u(const Desc &d, const RS_CONST KArgs
     }
 }
 
+typedef u32x4 u32x4_u __attribute__((aligned(1)));  // a 16-byte value at any byte address
+
+// Unit gather (see desc.h): per lane, 16-byte units of the segments' rows,
+// each one unaligned load and one unaligned store per receiver.  U units per
+// lane per pass, loads first.
+template <int L, int U>
+__device__ __forceinline__ void unit_addr(const Desc &d, const uint64_t *sp, const uint32_t *sst,
+                                          const uint32_t *scol, const uint32_t *sunit, uint32_t v,
+                                          const RS_GLOBAL unsigned char *&src, uint32_t &doff) {
+    const uint32_t upr = d.vpr, ns = d.pad[1], rb = d.run;
+    const uint32_t r = fastdiv(v, d.mul_vpr, d.sh_vpr);
+    const uint32_t j = v - r * upr;
+    uint32_t g = fastdiv(j, d.batch, d.pad[2]);
+    if (g >= ns) g = ns - 1;
+    while (g > 0 && j < sunit[g]) --g;
+    while (g + 1 < ns && j >= sunit[g + 1]) ++g;
+    const uint32_t w = (g + 1 < ns ? scol[g + 1] : rb) - scol[g];
+    const uint32_t k16 = 16u * (j - sunit[g]);
+    const uint32_t o = k16 < w - 16u ? k16 : w - 16u;
+    uint32_t i1, i2, i3;
+    row_indices<L>(d, d.ss[0] + r, i1, i2, i3);
+    src = (const RS_GLOBAL unsigned char *)(sp[g] + (i1 * sst[3 * g] + i2 * sst[3 * g + 1] + i3 * sst[3 * g + 2] + o));
+    doff = (r - d.ss[1]) * rb + scol[g] + o;
+}
+
+template <int L, int NPTR>
+__device__ __forceinline__ void run_gather_unit(const Desc &d, const RS_CONST KArgs<NPTR> *a) {
+    constexpr int U = 2;
+    const uint64_t *sp = reinterpret_cast<const uint64_t *>(rs_lds);
+    const uint32_t *sst = reinterpret_cast<const uint32_t *>(rs_lds + 8u * kMaxSegs);
+    const uint32_t *scol = reinterpret_cast<const uint32_t *>(rs_lds + 20u * kMaxSegs);
+    const uint32_t *sunit = reinterpret_cast<const uint32_t *>(rs_lds + 24u * kMaxSegs);
+    const RS_CONST int32_t *fan = (const RS_CONST int32_t *)(a->fan + d.fan_off);
+    const uint32_t nthr = blockDim.x;
+    for (uint32_t v = d.v0 + threadIdx.x; v < d.v1; v += U * nthr) {
+        u32x4 x[U];
+        uint32_t doff[U];
+#pragma unroll
+        for (int u = 0; u < U; ++u) {
+            const uint32_t vu = v + uint32_t(u) * nthr;
+            if (vu < d.v1) {
+                const RS_GLOBAL unsigned char *src;
+                unit_addr<L, U>(d, sp, sst, scol, sunit, vu, src, doff[u]);
+                x[u] = *(const RS_GLOBAL u32x4_u *)src;
+            }
+        }
+        for (uint32_t r = 0; r < d.nfan; ++r) {
+            RS_GLOBAL unsigned char *dst = (RS_GLOBAL unsigned char *)a->ptr[a->nsrc + uint32_t(fan[r])] + d.dst_base;
+#pragma unroll
+            for (int u = 0; u < U; ++u)
+                if (v + uint32_t(u) * nthr < d.v1) store_vec((RS_GLOBAL u32x4_u *)(dst + doff[u]), x[u]);
+        }
+    }
+}
+
 template <int L, int NPTR>
 __device__ __forceinline__ void run_gather_u_fan(const Desc &d, const RS_CONST KArgs<NPTR> *a) {
+    if (d.kind & kUnitGather) {
+        run_gather_unit<L>(d, a);
+        return;
+    }
     switch (d.nfan) {
         case 1: run_gather_u<L, 1>(d, a); break;
         case 2: run_gather_u<L, 2>(d, a); break;

@@ -756,6 +756,9 @@ bool lower_gather_group(Plan &p, const std::vector<size_t> &group, int64_t chunk
 #ifndef RS_UG_MIN_RUN
 #define RS_UG_MIN_RUN 2048u
 #endif
+#ifndef RS_UNIT_MAX_FAN
+#define RS_UNIT_MAX_FAN 2  // largest receiver count the unit gather takes
+#endif
 
 // Unaligned row gather of one group (see desc.h): segments of any widths of
 // at least 16 bytes tiling the destination row (one segment per row too,
@@ -906,8 +909,52 @@ bool lower_gather_unaligned(Plan &p, const std::vector<size_t> &group, int64_t c
         return false;
     }
     std::vector<Desc> mine;
-    mine.reserve(nchunks);
-    for (size_t k = 0; k < run_d0.size(); ++k) {
+    // One receiver and segments of at least 16 bytes: the unit gather
+    // (unaligned loads and stores, see desc.h).
+    bool unit = nfan <= int64_t(RS_UNIT_MAX_FAN);
+    uint32_t upr = 0;  // units per row
+    for (size_t k = 0; k < ns; ++k) {
+        const uint32_t w = (k + 1 < ns ? seg[k + 1].col : uint32_t(row_bytes)) - seg[k].col;
+        unit = unit && w >= 16;
+        seg[k].pad = upr;
+        upr += (w + 15) / 16;
+    }
+    if (unit) {
+        const uint64_t total = run_rows * upr;
+        if (total >= (uint64_t(1) << 32)) unit = false;
+    }
+    if (unit) {
+        const uint64_t total = run_rows * upr;
+        const uint64_t per = (total + cv - 1) / cv;
+        if (p.descs.size() + out.size() + per * run_d0.size() > kMaxDescs) {
+            p.too_many = true;
+            return false;
+        }
+        Desc u = d;
+        u.kind = uint8_t(make_kind(4, uint32_t(levels)) | kUnitGather);
+        u.vpr = upr;
+        const FastDiv fu = make_fastdiv(upr), fn = make_fastdiv(std::max<uint32_t>(1, upr / uint32_t(ns)));
+        u.mul_vpr = fu.mul;
+        u.sh_vpr = uint8_t(fu.shift);
+        u.batch = fn.mul;
+        u.pad[2] = fn.shift;
+        u.run = uint32_t(row_bytes);
+        for (size_t k = 0; k < run_d0.size(); ++k) {
+            for (uint64_t v0 = 0; v0 < total; v0 += cv) {
+                const uint64_t r_first = v0 / upr;
+                u.v0 = uint32_t(v0);
+                u.v1 = uint32_t(std::min(total, v0 + cv));
+                u.ss[0] = uint32_t(uint64_t(k) * run_rows);
+                u.ss[1] = uint32_t(r_first);
+                u.ss[2] = 0;
+                u.src_rel0 = 0;
+                u.dst_base = run_d0[k] + r_first * uint64_t(row_bytes);
+                mine.push_back(u);
+            }
+        }
+    }
+    if (!unit) mine.reserve(nchunks);
+    for (size_t k = 0; k < run_d0.size() && !unit; ++k) {
         const uint64_t rd0 = run_d0[k];  // this run's first byte
         const uint64_t s_first = rd0 / 16, s_end = (rd0 + run_bytes + 15) / 16;
         for (uint64_t s0 = s_first; s0 < s_end; s0 += cv) {

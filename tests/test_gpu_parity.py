@@ -364,9 +364,13 @@ def test_unaligned_gather_path(case):
         assert_same(got, want)
 
 
-@pytest.mark.parametrize("dm", [(1,), (2,)])
-@pytest.mark.parametrize("shape,n", [((2, 83, 390), 127), ((8, 21, 390), 128), ((13, 13, 390), 129),
-                                     ((2, 167, 390), 255), ((1, 337, 390), 257)])
+@pytest.mark.parametrize("shape,n,dm", [
+    # fan-out 2 (destination slots, 64 per 1 KiB chunk)
+    ((2, 83, 390), 127, (2,)), ((8, 21, 390), 128, (2,)), ((13, 13, 390), 129, (2,)),
+    ((2, 167, 390), 255, (2,)), ((1, 337, 390), 257, (2,)),
+    # fan-out 1 (unit gather: 32 segments of 2 units a row, one row per 1 KiB chunk)
+    ((1, 127, 390), 127, (1,)), ((2, 64, 390), 128, (1,)), ((1, 129, 390), 129, (1,)),
+    ((5, 51, 390), 255, (1,)), ((1, 257, 390), 257, (1,))])
 def test_unaligned_gather_chunk_counts_around_xcd_runs(shape, n, dm):
     """The unaligned row gather hands chunks to the XCDs in runs of 16, on a
     grid rounded up to whole rounds of 8 x 16 chunks: counts just below, at
