@@ -250,11 +250,13 @@ def main():
     # the chunks of each kind the plan holds; most workloads use one).
     n_gather, n_realign = B.reshard_plan_gather_chunks(plan), B.reshard_plan_realign_chunks(plan)
     n_gather_u = B.reshard_plan_unaligned_gather_chunks(plan)
+    n_unit = B.reshard_plan_unit_gather_chunks(plan)
     n_transpose = B.reshard_plan_transpose_chunks(plan)
     n_direct = st["n_descriptors"] - n_gather - n_gather_u - n_transpose - n_realign
+    n_slot = n_gather_u - n_unit
     kernel = max((n_direct, "reshard_kernel"), (n_gather, "reshard_gather_kernel"),
-                 (n_gather_u, "reshard_gather_u_kernel"), (n_transpose, "reshard_transpose_kernel"),
-                 (n_realign, "reshard_realign_kernel"))[1]
+                 (n_slot, "reshard_gather_u_kernel"), (n_unit, "reshard_gather_unit_kernel"),
+                 (n_transpose, "reshard_transpose_kernel"), (n_realign, "reshard_realign_kernel"))[1]
     out = {
         "metric": METRIC,
         "value": round(gbs, 2),
@@ -277,7 +279,7 @@ def main():
         },
         "pct_of_hbm_peak": round(100.0 * gbs / HBM_PEAK_GBS, 2),
         "roofline": {
-            "kernel": kernel, "launches_per_step": sum(1 for n in (n_direct, n_gather, n_gather_u, n_transpose, n_realign) if n)
+            "kernel": kernel, "launches_per_step": sum(1 for n in (n_direct, n_gather, n_slot, n_unit, n_transpose, n_realign) if n)
                                                         + (args.strategy == "allgather" and n_direct > 0),
             "bound": "hbm", "achieved": round(gbs, 2), "peak": HBM_PEAK_GBS, "unit": "GB/s",
             "frac": round(gbs / HBM_PEAK_GBS, 4), "traffic": traffic,

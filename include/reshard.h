@@ -301,6 +301,12 @@ int64_t reshard_plan_gather_chunks(const reshard_plan_t *plan);
  * RESHARD_NO_GATHER turns them off), or -1 for a NULL plan. */
 int64_t reshard_plan_unaligned_gather_chunks(const reshard_plan_t *plan);
 
+/* Of reshard_plan_unaligned_gather_chunks, the number that move 16-byte
+ * units of each segment with unaligned loads and stores (one or two
+ * receivers, every segment at least 16 bytes; a kernel of their own), or -1
+ * for a NULL plan. */
+int64_t reshard_plan_unit_gather_chunks(const reshard_plan_t *plan);
+
 /* Number of workgroup chunks that transpose tiles through LDS (tasks whose
  * source and destination layouts are contiguous along different tensor
  * dimensions), or -1 for a NULL plan. */

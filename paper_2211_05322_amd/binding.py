@@ -76,6 +76,8 @@ def load(path=None):
                                           _I32P, ctypes.c_int, _I64P, ctypes.c_char_p, _I32P, ctypes.c_uint,
                                           ctypes.POINTER(reshard_tuning_t), ctypes.POINTER(ctypes.c_void_p)]
     lib.reshard_plan_permuted.restype = ctypes.c_int
+    lib.reshard_plan_unit_gather_chunks.argtypes = [ctypes.c_void_p]
+    lib.reshard_plan_unit_gather_chunks.restype = ctypes.c_int64
     lib.reshard_plan_transpose_chunks.argtypes = [ctypes.c_void_p]
     lib.reshard_plan_transpose_chunks.restype = ctypes.c_int64
     lib.reshard_plan_ex.restype = ctypes.c_int
@@ -295,6 +297,10 @@ def reshard_plan_gather_chunks(plan):
 
 def reshard_plan_realign_chunks(plan):
     return int(load().reshard_plan_realign_chunks(plan.handle))
+
+
+def reshard_plan_unit_gather_chunks(plan):
+    return load().reshard_plan_unit_gather_chunks(plan.handle)
 
 
 def reshard_plan_transpose_chunks(plan):

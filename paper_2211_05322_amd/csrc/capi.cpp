@@ -285,6 +285,11 @@ int64_t reshard_plan_realign_chunks(const reshard_plan_t *plan) {
     return p ? int64_t(p->descs.size() - p->n_direct - p->n_gather - p->n_gather_u - p->n_transpose) : -1;
 }
 
+int64_t reshard_plan_unit_gather_chunks(const reshard_plan_t *plan) {
+    const rs::Plan *p = as_plan(plan);
+    return p ? int64_t(p->n_unit) : -1;
+}
+
 int64_t reshard_plan_transpose_chunks(const reshard_plan_t *plan) {
     const rs::Plan *p = as_plan(plan);
     return p ? int64_t(p->n_transpose) : -1;

@@ -119,9 +119,11 @@ static_assert(sizeof(Desc) == 112, "descriptor layout is shared by host and devi
 // vpr; ss[2] = reg_lo, src_rel0 = reg_hi: the chunk bytes [reg_lo, reg_hi)
 // belong to the group; run = nominal segment width (vpr / segments, a first
 // guess for the segment of a column) with batch/pad[2] its fast division;
-// pad[0], pad[1] the segment entries.  Each entry's `col` is its first byte
-// within the row; its src_base is the source offset of the group's first row
-// at that column (any byte alignment).
+// pad[0], pad[1] the segment entries; ds[0] = kUShortSegs when some segment
+// is shorter than 16 bytes (a slot may then hold three or more pieces).
+// Each entry's `col` is its first byte within the row; its src_base is the
+// source offset of the group's first row at that column (any byte
+// alignment).
 //
 // Unit gather (kind | kUnitGather, in the unaligned row-gather section, for
 // one receiver and segments of at least 16 bytes): lanes take 16-byte units
@@ -138,6 +140,7 @@ static_assert(sizeof(Desc) == 112, "descriptor layout is shared by host and devi
 // segment (a first guess); pad[0], pad[1] the segment entries, whose `pad`
 // holds the segment's first unit within the row.
 constexpr uint32_t kUnitGather = 0x08u;
+constexpr uint32_t kUShortSegs = 1u;
 struct Seg {
     uint64_t src_base;
     uint32_t ss[3];

@@ -572,7 +572,8 @@ __global__ __launch_bounds__(1024) void reshard_gather_kernel(KArgs<NPTR> args) 
 // byte of its piece, so no load leaves the 4 KiB page of a byte it needs.
 // LDS: 64-bit source pointers at 0, three strides per segment at
 // 8 * kMaxSegs, segment starts (bytes within the row) at 20 * kMaxSegs.
-constexpr uint32_t kGatherULds = 28u * kMaxSegs;  // + first units (unit gather) at 24 * kMaxSegs
+constexpr uint32_t kGatherULds = 24u * kMaxSegs;
+constexpr uint32_t kUnitLds = 28u * kMaxSegs;  // the same + first units at 24 * kMaxSegs
 
 // Chunk order of the unaligned row gather: the dispatcher hands workgroups to
 // the 8 XCDs in turn, so blocks b, b + 8, ..., b + 8 (kUGroup - 1) share an
@@ -588,7 +589,7 @@ __device__ __forceinline__ uint32_t grouped_chunk(uint32_t b) {
     return (b / (8u * kUGroup)) * (8u * kUGroup) + (b & 7u) * kUGroup + (b >> 3) % kUGroup;
 }
 
-template <int NPTR>
+template <int NPTR, bool UNITS = false>
 __device__ __forceinline__ void stage_segments_u(const Desc &d, const RS_CONST KArgs<NPTR> *a) {
     uint64_t *sp = reinterpret_cast<uint64_t *>(rs_lds);
     uint32_t *sst = reinterpret_cast<uint32_t *>(rs_lds + 8u * kMaxSegs);
@@ -600,7 +601,7 @@ __device__ __forceinline__ void stage_segments_u(const Desc &d, const RS_CONST K
         sst[3 * g + 1] = segs[g].ss[1];
         sst[3 * g + 2] = segs[g].ss[2];
         scol[g] = segs[g].col;
-        reinterpret_cast<uint32_t *>(rs_lds + 24u * kMaxSegs)[g] = segs[g].pad;
+        if (UNITS) reinterpret_cast<uint32_t *>(rs_lds + 24u * kMaxSegs)[g] = segs[g].pad;
     }
 }
 
@@ -632,7 +633,7 @@ struct USlot {
     uint32_t row, col, g;   // where the bytes from e2 on start (segments shorter than 16 bytes)
 };
 
-template <int L>
+template <int L, bool SHORT>
 __device__ __forceinline__ void uslot_load(const Desc &d, const uint64_t *sp, const uint32_t *sst,
                                            const uint32_t *scol, uint32_t c0, USlot &s) {
     const u32x4 z = {0u, 0u, 0u, 0u};
@@ -668,13 +669,16 @@ __device__ __forceinline__ void uslot_load(const Desc &d, const uint64_t *sp, co
             col = send;
             ++g;
         }
-        const uint32_t send2 = g + 1 < ns ? scol[g + 1] : rb;
-        s.e2 = s.e1 + ((s.hi - s.e1) < (send2 - col) ? (s.hi - s.e1) : (send2 - col));
+        uint32_t send2 = rb;
+        if (SHORT) {  // piece 2 may end before the slot does
+            send2 = g + 1 < ns ? scol[g + 1] : rb;
+            s.e2 = s.e1 + ((s.hi - s.e1) < (send2 - col) ? (s.hi - s.e1) : (send2 - col));
+        }
         q = segment_addr<L>(d, sp, sst, scol, g, row, col);
         s.shb = uint32_t(q) & 15u;
         s.b0 = load_vec((const RS_GLOBAL u32x4 *)(q & ~uint64_t(15)));
         if (s.shb + (s.e2 - s.e1) > 16u) s.b1 = load_vec((const RS_GLOBAL u32x4 *)((q & ~uint64_t(15)) + 16u));
-        if (s.e2 < s.hi) {  // a short segment: the bytes from e2 on come from the pieces after it
+        if (SHORT && s.e2 < s.hi) {  // a short segment: the bytes from e2 on come from the pieces after it
             if (send2 == rb) {
                 ++row;
                 col = 0;
@@ -763,8 +767,9 @@ __device__ __forceinline__ void uslot_store(RS_GLOBAL unsigned char *slot, u32x4
 }
 
 // RF > 0: compile-time receiver count (vector-major stores up to 4
-// receivers, as the aligned gather); RF == 0: runtime count.
-template <int L, int RF, int NPTR>
+// receivers, as the aligned gather); RF == 0: runtime count.  SHORT: the
+// group has segments shorter than 16 bytes.
+template <int L, int RF, bool SHORT, int NPTR>
 __device__ __forceinline__ void run_gather_u(const Desc &d, const RS_CONST KArgs<NPTR> *a) {
     const uint64_t *sp = reinterpret_cast<const uint64_t *>(rs_lds);
     const uint32_t *sst = reinterpret_cast<const uint32_t *>(rs_lds + 8u * kMaxSegs);
@@ -776,12 +781,14 @@ __device__ __forceinline__ void run_gather_u(const Desc &d, const RS_CONST KArgs
         const uint32_t c0 = 16u * ls, c1 = c0 + 16u * nthr;
         const bool has1 = ls + nthr < n;
         USlot s0, s1;
-        uslot_load<L>(d, sp, sst, scol, c0, s0);
-        if (has1) uslot_load<L>(d, sp, sst, scol, c1, s1);
+        uslot_load<L, SHORT>(d, sp, sst, scol, c0, s0);
+        if (has1) uslot_load<L, SHORT>(d, sp, sst, scol, c1, s1);
         u32x4 o0 = uslot_compose(s0, c0);
         u32x4 o1 = has1 ? uslot_compose(s1, c1) : o0;
-        if (s0.e2 < s0.hi) o0 = uslot_rest<L>(d, sp, sst, scol, s0, c0, o0);
-        if (has1 && s1.e2 < s1.hi) o1 = uslot_rest<L>(d, sp, sst, scol, s1, c1, o1);
+        if (SHORT) {
+            if (s0.e2 < s0.hi) o0 = uslot_rest<L>(d, sp, sst, scol, s0, c0, o0);
+            if (has1 && s1.e2 < s1.hi) o1 = uslot_rest<L>(d, sp, sst, scol, s1, c1, o1);
+        }
         if constexpr (RF >= 1 && RF <= 4) {
 #pragma unroll
             for (uint32_t r = 0; r < nr; ++r)
@@ -868,20 +875,20 @@ __device__ __forceinline__ void run_gather_unit(const Desc &d, const RS_CONST KA
 
 template <int L, int NPTR>
 __device__ __forceinline__ void run_gather_u_fan(const Desc &d, const RS_CONST KArgs<NPTR> *a) {
-    if (d.kind & kUnitGather) {
-        run_gather_unit<L>(d, a);
+    if (d.ds[0] & kUShortSegs) {  // rare: one runtime-count form
+        run_gather_u<L, 0, true>(d, a);
         return;
     }
     switch (d.nfan) {
-        case 1: run_gather_u<L, 1>(d, a); break;
-        case 2: run_gather_u<L, 2>(d, a); break;
-        case 3: run_gather_u<L, 3>(d, a); break;
-        case 4: run_gather_u<L, 4>(d, a); break;
-        case 5: run_gather_u<L, 5>(d, a); break;
-        case 6: run_gather_u<L, 6>(d, a); break;
-        case 7: run_gather_u<L, 7>(d, a); break;
-        case 8: run_gather_u<L, 8>(d, a); break;
-        default: run_gather_u<L, 0>(d, a); break;
+        case 1: run_gather_u<L, 1, false>(d, a); break;
+        case 2: run_gather_u<L, 2, false>(d, a); break;
+        case 3: run_gather_u<L, 3, false>(d, a); break;
+        case 4: run_gather_u<L, 4, false>(d, a); break;
+        case 5: run_gather_u<L, 5, false>(d, a); break;
+        case 6: run_gather_u<L, 6, false>(d, a); break;
+        case 7: run_gather_u<L, 7, false>(d, a); break;
+        case 8: run_gather_u<L, 8, false>(d, a); break;
+        default: run_gather_u<L, 0, false>(d, a); break;
     }
 }
 
@@ -1060,6 +1067,24 @@ __global__ __launch_bounds__(256) void reshard_transpose_kernel(KArgs<NPTR> args
     }
 }
 
+// Unit-gather chunks in their own kernel, so the slot kernel keeps its
+// registers (measured: sharing one kernel slowed the slot path 12-27 %).
+template <int NPTR>
+__global__ __launch_bounds__(256) void reshard_gather_unit_kernel(KArgs<NPTR> args) {
+    const RS_CONST KArgs<NPTR> *a = (const RS_CONST KArgs<NPTR> *)__builtin_amdgcn_kernarg_segment_ptr();
+    const uint32_t b = blockIdx.x;
+    const uint32_t idx = a->per_xcd ? (b & 7u) * a->per_xcd + (b >> 3) : grouped_chunk(b);
+    if (idx >= a->ndesc) return;
+    const Desc d = load_desc(a, idx);
+    stage_segments_u<NPTR, true>(d, a);
+    __syncthreads();
+    switch (kind_levels(d.kind)) {
+        case 1: run_gather_unit<1>(d, a); break;
+        case 2: run_gather_unit<2>(d, a); break;
+        default: run_gather_unit<3>(d, a); break;
+    }
+}
+
 // Realignment chunks run in their own kernel so their register use does not
 // bound the direct kernel's occupancy.  STAGE: through LDS, else shifted loads.
 template <int NPTR, bool STAGE>
@@ -1219,24 +1244,34 @@ reshard_status_t launch(const Plan &p, const Desc *descs, const int32_t *fan, co
         const reshard_status_t st = launch_one(reshard_gather_kernel<NPTR>, a, n_gather, remap, block, glds, stream);
         if (st != RESHARD_OK) return st;
     }
-    if (n_gather_u) {
-        uint32_t ulds = user_lds;
-        if (p.tuning.cap_is_default) {
-            // Rows gathered from several senders: about 64 receiver write
-            // streams per CU, as the aligned gather.  One sender per row
-            // (rows in runs, or whole rows in another phase) reads like the
-            // direct kernel and wants its caps: measured uncapped best at
-            // fan-out 1, 16 waves at 2 (10 % faster than uncapped), 8 at 4
-            // (12 % faster than 16).
-            const uint32_t fan = uint32_t(p.gather_u_fanout > 0 ? p.gather_u_fanout : 1);
-            uint32_t waves = 64u / fan > 8u ? 64u / fan : 8u;
-            if (p.gather_u_segs == 1) waves = fan <= 1 ? 32u : fan == 2 ? 16u : 8u;
-            ulds = residency_lds(waves, block < 256u ? block : 256u);
-        }
+    // the unaligned row-gather section: slot chunks, then unit chunks
+    const uint32_t n_unit = uint32_t(p.n_unit), n_slot = n_gather_u - n_unit;
+    // Rows gathered from several senders: about 64 receiver write streams
+    // per CU, as the aligned gather.  One sender per row (rows in runs, or
+    // whole rows in another phase) reads like the direct kernel and wants
+    // its caps: measured uncapped best at fan-out 1, 16 waves at 2 (10 %
+    // faster than uncapped), 8 at 4 (12 % faster than 16).
+    auto gather_u_lds = [&](int64_t fanout, int64_t segs) {
+        if (!p.tuning.cap_is_default) return user_lds;
+        const uint32_t fan = uint32_t(fanout > 0 ? fanout : 1);
+        uint32_t waves = 64u / fan > 8u ? 64u / fan : 8u;
+        if (segs == 1) waves = fan <= 1 ? 32u : fan == 2 ? 16u : 8u;
+        return residency_lds(waves, block < 256u ? block : 256u);
+    };
+    if (n_slot) {
+        const uint32_t ulds = gather_u_lds(p.gather_u_fanout, p.gather_u_segs);
         a.descs = descs + n_direct + n_gather;
-        const reshard_status_t st = launch_one(reshard_gather_u_kernel<NPTR>, a, n_gather_u, remap,
+        const reshard_status_t st = launch_one(reshard_gather_u_kernel<NPTR>, a, n_slot, remap,
                                                block < 256u ? block : 256u,
                                                ulds > kGatherULds ? ulds : kGatherULds, stream, 8u * kUGroup);
+        if (st != RESHARD_OK) return st;
+    }
+    if (n_unit) {
+        const uint32_t ulds = gather_u_lds(p.unit_fanout, p.unit_segs);
+        a.descs = descs + n_direct + n_gather + n_slot;
+        const reshard_status_t st = launch_one(reshard_gather_unit_kernel<NPTR>, a, n_unit, remap,
+                                               block < 256u ? block : 256u, ulds > kUnitLds ? ulds : kUnitLds,
+                                               stream, 8u * kUGroup);
         if (st != RESHARD_OK) return st;
     }
     if (n_transpose) {

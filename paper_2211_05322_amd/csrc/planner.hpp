@@ -79,7 +79,8 @@ struct Plan {
     uint32_t lds_bytes = 0;    // LDS the realignment chunks need per workgroup
     size_t n_direct = 0;       // descs[0, n_direct): direct chunks
     size_t n_gather = 0;       // descs[n_direct, n_direct + n_gather): row-gather chunks;
-    size_t n_gather_u = 0;     // then n_gather_u unaligned row-gather chunks;
+    size_t n_gather_u = 0;     // then n_gather_u unaligned row-gather chunks (the last n_unit
+    size_t n_unit = 0;         // of them unit-gather chunks, their own kernel);
     size_t n_transpose = 0;    // then n_transpose tile-transpose chunks;
     uint32_t transpose_rows = 0;  // rows of the widest transpose tile (LDS: rows x 128 bytes)
                                // the rest: realignment chunks
@@ -87,6 +88,8 @@ struct Plan {
     int64_t gather_fanout = 0; // largest receiver count among row-gather chunks
     int64_t gather_u_fanout = 0; // ... among unaligned row-gather chunks
     int64_t gather_u_segs = 0;   // most segments per row among unaligned row-gather groups
+    int64_t unit_fanout = 0;     // ... and among the unit-gather groups:
+    int64_t unit_segs = 0;       //     receivers, segments per row
     int64_t direct_fanout = 0; // largest receiver count among direct chunks
     size_t n_phase1 = 0;       // descs[0, n_phase1) run before descs[n_phase1, n_direct)
                                // (two launches; only the all-gather strategy has a second phase)

@@ -3,8 +3,9 @@
     python -m paper_2211_05322_amd.workload_report [--steps 50] [--flush-steps 20] [--flush-mib 1024]
 
 For each workload (the five resharding tasks, workloads 5 and 3 with an
-uneven last dimension, misaligned rows that arrive in runs, then the
-one-sender replication microbenchmark at 1, 4 and 8 receivers) prints one
+uneven last dimension, misaligned rows that arrive in runs, workloads 2 and 5
+with the destination buffers transposed, then the one-sender replication
+microbenchmark at 1, 4 and 8 receivers) prints one
 markdown row: unit tasks, fan-out, chunks per kernel, bytes moved (read +
 write), planning time, and four timings of `reshard_execute`:
 
@@ -84,16 +85,21 @@ def _time_cold(fn, steps, scratch, stream):
 def report_row(key, w, steps, flush_steps, scratch, stream):
     x = make_workload_tensor(w, seed=0, device="cuda")
     rep = "R" * len(w.shape)
-    scatter = B.reshard_plan(w.shape, w.dtype, (1,), rep, w.src_mesh, w.src_spec, block_threads=1024)
+    # setup and check plans run 128-thread workgroups (told apart from the
+    # timed plan's in kernel traces)
+    scatter = B.reshard_plan(w.shape, w.dtype, (1,), rep, w.src_mesh, w.src_spec, block_threads=128,
+                             dst_perm=w.src_perm)
     src = B.empty_shards(scatter, 1)
     B.reshard_execute(scatter, [x], src)
     t0 = time.perf_counter()
-    plan = B.reshard_plan(w.shape, w.dtype, w.src_mesh, w.src_spec, w.dst_mesh, w.dst_spec)
+    plan = B.reshard_plan(w.shape, w.dtype, w.src_mesh, w.src_spec, w.dst_mesh, w.dst_spec, src_perm=w.src_perm,
+                          dst_perm=w.dst_perm)
     plan_ms = (time.perf_counter() - t0) * 1e3
     st = B.reshard_plan_stats(plan)
     n_gather, n_realign = B.reshard_plan_gather_chunks(plan), B.reshard_plan_realign_chunks(plan)
     n_gather_u = B.reshard_plan_unaligned_gather_chunks(plan)
-    n_direct = st["n_descriptors"] - n_gather - n_gather_u - n_realign
+    n_transpose = B.reshard_plan_transpose_chunks(plan)
+    n_direct = st["n_descriptors"] - n_gather - n_gather_u - n_transpose - n_realign
     dst = B.empty_shards(plan, 1)
     sp0, dp0 = B.pointer_array(src), B.pointer_array(dst)  # built once, as a caller's loop would
     run = lambda: B.reshard_execute(plan, sp0, dp0, stream=stream)  # noqa: E731
@@ -124,14 +130,16 @@ def report_row(key, w, steps, flush_steps, scratch, stream):
     torch.cuda.synchronize()
     rot_us = _time_back_to_back(run_rot, max(steps, 2 * nsets), stream)
     del sets, ptrs
-    back_plan = B.reshard_plan(w.shape, w.dtype, w.dst_mesh, w.dst_spec, (1,), rep, block_threads=1024)
+    back_plan = B.reshard_plan(w.shape, w.dtype, w.dst_mesh, w.dst_spec, (1,), rep, block_threads=128,
+                               src_perm=w.dst_perm)
     back = B.empty_shards(back_plan, 1)
     B.reshard_execute(back_plan, dst, back)
     torch.cuda.synchronize()
     ok = bool(torch.equal(back[0].view(torch.uint8), x.view(torch.uint8)))
     moved = st["bytes_read"] + st["bytes_written"]
     gbs = lambda us: moved / us / 1e3  # noqa: E731
-    kinds = "/".join(str(n) for n in (n_direct, n_gather, n_gather_u, n_realign))
+    n_unit = B.reshard_plan_unit_gather_chunks(plan)
+    kinds = "/".join(str(n) for n in (n_direct, n_gather, n_gather_u - n_unit, n_unit, n_transpose, n_realign))
     row = (f"| {key} | {w.name} | {st['n_unit_tasks']} | {st['max_fanout']} | {kinds} | {moved / 1e6:.1f} | "
            f"{plan_ms:.2f} | {warm_us:.1f} | {100 * gbs(warm_us) / HBM_PEAK_GBS:.1f} | "
            f"{rot_us:.1f} ({nsets}) | {100 * gbs(rot_us) / HBM_PEAK_GBS:.1f} | "
@@ -147,7 +155,8 @@ def main():
     ap.add_argument("--steps", type=int, default=50)
     ap.add_argument("--flush-steps", type=int, default=20)
     ap.add_argument("--flush-mib", type=int, default=1024)
-    ap.add_argument("--workloads", default="1,2,3,4,5,uneven5,uneven3,runs1,runs2,runs4,fanout1,fanout4,fanout8")
+    ap.add_argument("--workloads", default="1,2,3,4,5,uneven5,uneven3,runs1,runs2,runs4,transposed2,transposed5,"
+                                           "fanout1,fanout4,fanout8")
     a = ap.parse_args()
     if not torch.cuda.is_available():
         raise SystemExit("no GPU visible")
@@ -159,9 +168,10 @@ def main():
           f"over (n) buffer sets in turn; cold: mean of {a.flush_steps} launches, each after a read of "
           f"{a.flush_mib} MiB; graph: per reshard, 50 captured executes replayed; % of "
           f"{HBM_PEAK_GBS:.0f} GB/s\n")
-    print("| id | workload | unit tasks | fan-out | chunks direct/gather/unaligned gather/realign | MB moved | plan ms | "
+    print("| id | workload | unit tasks | fan-out | chunks direct/gather/unaligned gather (slots/units)/transpose/realign | MB moved | "
+          "plan ms | "
           "back-to-back µs | % | rotated µs (n) | % | cold µs | % | round trip | graph µs |")
-    print("|---" * 15 + "|")
+    print("|---" * 15 + "|")  # (the chunks column lists six counts)
     all_ok = True
     for key in a.workloads.split(","):
         w = workload_by_name(key)
