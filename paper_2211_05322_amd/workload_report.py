@@ -155,7 +155,7 @@ def main():
     ap.add_argument("--steps", type=int, default=50)
     ap.add_argument("--flush-steps", type=int, default=20)
     ap.add_argument("--flush-mib", type=int, default=1024)
-    ap.add_argument("--workloads", default="1,2,3,4,5,uneven5,uneven3,runs1,runs2,runs4,transposed2,transposed5,"
+    ap.add_argument("--workloads", default="1,2,3,4,5,uneven5,uneven3,uneven5_1rep,runs1,runs2,runs4,transposed2,transposed5,"
                                            "fanout1,fanout4,fanout8")
     a = ap.parse_args()
     if not torch.cuda.is_available():

@@ -72,6 +72,10 @@ UNEVEN_WORKLOADS = {
                         "normal", (4, 8), "R R S^{01}", (4, 8), "R S^1 R"),
     "uneven3": Workload("fp16_16x2048x5130_s01_uneven_to_replicated", (16, 2048, 5130), "float16", "normal",
                         (2, 4), "R R S^{01}", (2, 4), "R R R"),
+    # uneven workload 5 to one replica: 32 senders per destination row at
+    # fan-out 1 (the unit gather)
+    "uneven5_1rep": Workload("gpt3_act_fp16_8x2048x12300_hidden32_uneven_to_seq8_1rep", (8, 2048, 12300), "float16",
+                             "normal", (4, 8), "R R S^{01}", (1, 8), "R S^1 R"),
     # the middle dimension split 1024/1023 on the source and the outer one on
     # the destination, with 24602-byte rows: destination rows contiguous only
     # in runs of 1024 or 1023, in different 16-byte phases; fan-out 1, 2, 4
