@@ -759,6 +759,9 @@ bool lower_gather_group(Plan &p, const std::vector<size_t> &group, int64_t chunk
 #ifndef RS_UNIT_MAX_FAN
 #define RS_UNIT_MAX_FAN 1  // largest receiver count the unit gather takes
 #endif
+#ifndef RS_UNIT_MAX_SEG
+#define RS_UNIT_MAX_SEG 2048  // the unit gather takes mean segment widths below this (bytes)
+#endif
 
 // Unaligned row gather of one group (see desc.h): segments of any widths of
 // at least 16 bytes tiling the destination row (one segment per row too,
@@ -910,11 +913,13 @@ bool lower_gather_unaligned(Plan &p, const std::vector<size_t> &group, int64_t c
         return false;
     }
     std::vector<Desc> mine;
-    // One receiver, several senders per row and segments of at least 16
-    // bytes: the unit gather (unaligned loads and stores, see desc.h).
-    // Measured against destination slots: 8 % faster with 32 senders at
-    // fan-out 1; slower at fan-out 2 and with one sender per row.
-    bool unit = nfan <= int64_t(RS_UNIT_MAX_FAN) && ns >= 2;
+    // One receiver, segments of at least 16 bytes and under RS_UNIT_MAX_SEG
+    // on average: the unit gather (unaligned loads and stores, see desc.h).
+    // The slot form spends its time on slots that straddle two segments
+    // (or rows), which short segments make frequent.  Measured against
+    // destination slots: 8 % faster with 770-byte segments at fan-out 1;
+    // slower at fan-out 2 and with rows of 6 KiB and more from one sender.
+    bool unit = nfan <= int64_t(RS_UNIT_MAX_FAN) && row_bytes < int64_t(RS_UNIT_MAX_SEG) * int64_t(ns);
     uint32_t upr = 0;  // units per row
     for (size_t k = 0; k < ns; ++k) {
         const uint32_t w = (k + 1 < ns ? seg[k + 1].col : uint32_t(row_bytes)) - seg[k].col;
