@@ -843,9 +843,13 @@ __device__ __forceinline__ void unit_addr(const Desc &d, const uint64_t *sp, con
     doff = (r - d.ss[1]) * rb + scol[g] + o;
 }
 
+#ifndef RS_UNIT_U
+#define RS_UNIT_U 2
+#endif
+
 template <int L, int NPTR>
 __device__ __forceinline__ void run_gather_unit(const Desc &d, const RS_CONST KArgs<NPTR> *a) {
-    constexpr int U = 2;
+    constexpr int U = RS_UNIT_U;  // units per lane per pass, loads first
     const uint64_t *sp = reinterpret_cast<const uint64_t *>(rs_lds);
     const uint32_t *sst = reinterpret_cast<const uint32_t *>(rs_lds + 8u * kMaxSegs);
     const uint32_t *scol = reinterpret_cast<const uint32_t *>(rs_lds + 20u * kMaxSegs);

@@ -532,10 +532,15 @@ void emit_transpose(Plan &p, const TPiece &tp, int32_t src_buf, int64_t fan_off,
     const int nl = int(tp.outer.size());
     const Level o1 = nl >= 1 ? tp.outer[size_t(nl - 1)] : Level{1, 0, 0};
     const Level o2 = nl >= 2 ? tp.outer[0] : Level{1, 0, 0};
-    // tile width along B: up to 4 x 128 bytes, enough for the B extent, with
-    // at most 256 tile rows (32 KiB of LDS)
+    // tile width along B: the narrowest of 1, 2, 4 x 128 bytes that covers
+    // the whole B extent (a tile then writes whole destination rows), with at
+    // most 256 tile rows (32 KiB of LDS); B extents wider than that take
+    // 2 x 128 bytes, which keeps twice the tiles resident (measured: 512-byte
+    // rows 382.6 us at 512-byte tiles against 391.6 at 256; 1 KiB rows 24.4
+    // against 26.2 us the other way)
     uint32_t wide = 0;
-    while (wide < RS_TMAXW_LOG2 && (te << wide) * es < tp.nb * es && (te << (wide + 1)) <= 256) ++wide;
+    while (wide < RS_TMAXW_LOG2 && (te << wide) < tp.nb && (te << (wide + 1)) <= 256) ++wide;
+    if ((te << wide) < tp.nb && wide > 1) wide = 1;
     const int64_t tr = te << wide;
     const uint64_t ntb = uint64_t((tp.nb + tr - 1) / tr), nta = uint64_t((tp.na + te - 1) / te);
     const uint64_t tiles = ntb * nta * uint64_t(o1.n) * uint64_t(o2.n);
