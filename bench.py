@@ -122,6 +122,9 @@ def main():
     ap.add_argument("--calib-copy-mib", type=int, default=0,
                     help="after timing, run a plain device copy of this many MiB 3 times "
                          "(a known-size kernel for hardware counter calibration)")
+    ap.add_argument("--calib-fill-mib", type=int, default=0,
+                    help="after timing, fill one buffer of this many MiB 3 times with the HIP runtime's "
+                         "hipMemsetD32Async (its write form, for comparison in kernel traces and counters)")
     args = ap.parse_args()
 
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
@@ -241,6 +244,20 @@ def main():
             c.copy_(a)
         torch.cuda.synchronize()
         del a, c
+    if args.calib_fill_mib:
+        import ctypes
+        hip = ctypes.CDLL("libamdhip64.so")
+        hip.hipMemsetD32Async.argtypes = [ctypes.c_void_p, ctypes.c_int, ctypes.c_size_t, ctypes.c_void_p]
+        hip.hipMemsetD32Async.restype = ctypes.c_int
+        n = args.calib_fill_mib << 20
+        c = torch.empty(n, dtype=torch.uint8, device="cuda")
+        torch.cuda.synchronize()
+        for _ in range(3):
+            rc = hip.hipMemsetD32Async(ctypes.c_void_p(c.data_ptr()), 7, n // 4, ctypes.c_void_p(stream.cuda_stream))
+            if rc != 0:
+                raise RuntimeError(f"hipMemsetD32Async failed ({rc})")
+        torch.cuda.synchronize()
+        del c
     # the counter record holds the default tuning only
     tuned = args.chunk_bytes or args.block_threads or args.max_wgs_per_cu
     traffic = None if tuned else measured_traffic(traffic_key(w.name, args.flags, args.strategy),
