@@ -439,8 +439,10 @@ reshard_status_t reshard_debug_execute_host(const reshard_plan_t *plan, void *co
                         while (g > 0 && j < sg[g].pad) --g;
                         while (g + 1 < ns && j >= sg[g + 1].pad) ++g;
                         const uint32_t w = (g + 1 < ns ? sg[g + 1].col : rbytes) - sg[g].col;
-                        if (w < 16) return fail(RESHARD_EINVAL, "internal: unit gather segment under 16 bytes");
-                        const uint32_t o = std::min(16u * (j - sg[g].pad), w - 16u);
+                        if (w < 16 && !(d.ds[0] & rs::kUShortSegs))
+                            return fail(RESHARD_EINVAL, "internal: unit gather segment under 16 bytes, unflagged");
+                        const uint32_t n = std::min(w, 16u);  // a segment under 16 bytes is one unit
+                        const uint32_t o = w < 16 ? 0u : std::min(16u * (j - sg[g].pad), w - 16u);
                         uint8_t out[16];
                         uint32_t i1 = 0, i2 = 0, i3 = 0;
                         if (levels == 1) rs::row_indices<1>(d, d.ss[0] + r, i1, i2, i3);
@@ -448,15 +450,15 @@ reshard_status_t reshard_debug_execute_host(const reshard_plan_t *plan, void *co
                         else rs::row_indices<3>(d, d.ss[0] + r, i1, i2, i3);
                         const uint64_t q = sg[g].src_base + uint32_t(i1 * sg[g].ss[0] + i2 * sg[g].ss[1] +
                                                                      i3 * sg[g].ss[2] + o);
-                        if (o + 16 > w || q + 16 > uint64_t(p->src_local_numel[sg[g].buf] * p->es))
+                        if (o + n > w || q + n > uint64_t(p->src_local_numel[sg[g].buf] * p->es))
                             return fail(RESHARD_EINVAL, "internal: unit gather load outside its segment or shard");
-                        std::memcpy(out, static_cast<const char *>(src_ptrs[sg[g].buf]) + q, 16);
+                        std::memcpy(out, static_cast<const char *>(src_ptrs[sg[g].buf]) + q, n);
                         const uint64_t doff = uint64_t((r - d.ss[1]) * rbytes + sg[g].col + o);
                         for (uint32_t q = 0; q < d.nfan; ++q) {
                             const int32_t dev = p->fan[d.fan_off + q];
-                            if (d.dst_base + doff + 16 > uint64_t(p->dst_local_numel[dev] * p->es))
+                            if (d.dst_base + doff + n > uint64_t(p->dst_local_numel[dev] * p->es))
                                 return fail(RESHARD_EINVAL, "internal: unit gather store outside its destination shard");
-                            std::memcpy(static_cast<char *>(dst_ptrs[dev]) + d.dst_base + doff, out, 16);
+                            std::memcpy(static_cast<char *>(dst_ptrs[dev]) + d.dst_base + doff, out, n);
                         }
                     }
                     continue;

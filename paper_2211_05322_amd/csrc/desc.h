@@ -126,12 +126,13 @@ static_assert(sizeof(Desc) == 112, "descriptor layout is shared by host and devi
 // alignment).
 //
 // Unit gather (kind | kUnitGather, in the unaligned row-gather section, for
-// one receiver and segments of at least 16 bytes): lanes take 16-byte units
-// of each segment's row rather than slots of the destination -- unit k of a
-// segment of width w covers bytes [min(16k, w - 16), +16), so the last unit
-// overlaps the one before it and rewrites the same bytes -- each one
-// unaligned 16-byte load and one unaligned 16-byte store, with no shifts or
-// merges.  Fields: v0, v1 = units [v0, v1) of the region (unit v is unit
+// one receiver): lanes take 16-byte units of each segment's row rather than
+// slots of the destination -- unit k of a segment of width w covers bytes
+// [min(16k, w - 16), +16), so the last unit overlaps the one before it and
+// rewrites the same bytes -- each one unaligned 16-byte load and one
+// unaligned 16-byte store, with no shifts or merges.  A segment shorter
+// than 16 bytes is one unit of w bytes, loaded from the aligned words that
+// hold it and stored byte by byte; ds[0] = kUShortSegs marks such groups.  Fields: v0, v1 = units [v0, v1) of the region (unit v is unit
 // v mod vpr of region row v / vpr); vpr = units per row with mul_vpr /
 // sh_vpr; n1, n2 and their multipliers = the source levels; ss[0] = the
 // region's first row in group numbering, ss[1] = the chunk's first region

@@ -822,11 +822,12 @@ typedef u32x4 u32x4_u __attribute__((aligned(1)));  // a 16-byte value at any by
 
 // Unit gather (see desc.h): per lane, 16-byte units of the segments' rows,
 // each one unaligned load and one unaligned store per receiver.  U units per
-// lane per pass, loads first.
+// lane per pass, loads first.  w: the unit's segment width (a segment under
+// 16 bytes is one unit of w bytes).
 template <int L, int U>
 __device__ __forceinline__ void unit_addr(const Desc &d, const uint64_t *sp, const uint32_t *sst,
                                           const uint32_t *scol, const uint32_t *sunit, uint32_t v,
-                                          const RS_GLOBAL unsigned char *&src, uint32_t &doff) {
+                                          const RS_GLOBAL unsigned char *&src, uint32_t &doff, uint32_t &w) {
     const uint32_t upr = d.vpr, ns = d.pad[1], rb = d.run;
     const uint32_t r = fastdiv(v, d.mul_vpr, d.sh_vpr);
     const uint32_t j = v - r * upr;
@@ -834,9 +835,9 @@ __device__ __forceinline__ void unit_addr(const Desc &d, const uint64_t *sp, con
     if (g >= ns) g = ns - 1;
     while (g > 0 && j < sunit[g]) --g;
     while (g + 1 < ns && j >= sunit[g + 1]) ++g;
-    const uint32_t w = (g + 1 < ns ? scol[g + 1] : rb) - scol[g];
+    w = (g + 1 < ns ? scol[g + 1] : rb) - scol[g];
     const uint32_t k16 = 16u * (j - sunit[g]);
-    const uint32_t o = k16 < w - 16u ? k16 : w - 16u;
+    const uint32_t o = w < 16u ? 0u : k16 < w - 16u ? k16 : w - 16u;
     uint32_t i1, i2, i3;
     row_indices<L>(d, d.ss[0] + r, i1, i2, i3);
     src = (const RS_GLOBAL unsigned char *)(sp[g] + (i1 * sst[3 * g] + i2 * sst[3 * g + 1] + i3 * sst[3 * g + 2] + o));
@@ -847,7 +848,30 @@ __device__ __forceinline__ void unit_addr(const Desc &d, const uint64_t *sp, con
 #define RS_UNIT_U 2
 #endif
 
-template <int L, int NPTR>
+// The n (< 16) bytes at q as the low bytes of a 16-byte value: the one or
+// two aligned words that hold them, funnel-shifted (an aligned word holding
+// one byte of a buffer lies inside the buffer's allocation).
+__device__ __forceinline__ u32x4 load_short(const RS_GLOBAL unsigned char *q, uint32_t n) {
+    const uint64_t a = uint64_t(q);
+    const uint32_t sh = uint32_t(a) & 15u;
+    const RS_GLOBAL u32x4 *w = (const RS_GLOBAL u32x4 *)(a & ~uint64_t(15));
+    const u32x4 z = {0u, 0u, 0u, 0u};
+    const u32x4 w0 = w[0];
+    const u32x4 w1 = sh + n > 16u ? w[1] : z;
+    return funnel32(w0, w1, sh);
+}
+
+// The low n (< 16) bytes of v to q, one byte store each.
+__device__ __forceinline__ void store_short(RS_GLOBAL unsigned char *q, u32x4 v, uint32_t n) {
+    const uint32_t x[4] = {v.x, v.y, v.z, v.w};
+#pragma unroll
+    for (uint32_t i = 0; i < 15u; ++i)
+        if (i < n) q[i] = (unsigned char)(x[i >> 2] >> (8u * (i & 3u)));
+}
+
+// SHORT: the group has segments shorter than 16 bytes (each one unit, moved
+// by load_short / store_short).
+template <int L, bool SHORT, int NPTR>
 __device__ __forceinline__ void run_gather_unit(const Desc &d, const RS_CONST KArgs<NPTR> *a) {
     constexpr int U = RS_UNIT_U;  // units per lane per pass, loads first
     const uint64_t *sp = reinterpret_cast<const uint64_t *>(rs_lds);
@@ -858,21 +882,25 @@ __device__ __forceinline__ void run_gather_unit(const Desc &d, const RS_CONST KA
     const uint32_t nthr = blockDim.x;
     for (uint32_t v = d.v0 + threadIdx.x; v < d.v1; v += U * nthr) {
         u32x4 x[U];
-        uint32_t doff[U];
+        uint32_t doff[U], w[U];
 #pragma unroll
         for (int u = 0; u < U; ++u) {
             const uint32_t vu = v + uint32_t(u) * nthr;
             if (vu < d.v1) {
                 const RS_GLOBAL unsigned char *src;
-                unit_addr<L, U>(d, sp, sst, scol, sunit, vu, src, doff[u]);
-                x[u] = *(const RS_GLOBAL u32x4_u *)src;
+                unit_addr<L, U>(d, sp, sst, scol, sunit, vu, src, doff[u], w[u]);
+                if (!SHORT || w[u] >= 16u) x[u] = *(const RS_GLOBAL u32x4_u *)src;
+                else x[u] = load_short(src, w[u]);
             }
         }
         for (uint32_t r = 0; r < d.nfan; ++r) {
             RS_GLOBAL unsigned char *dst = (RS_GLOBAL unsigned char *)a->ptr[a->nsrc + uint32_t(fan[r])] + d.dst_base;
 #pragma unroll
-            for (int u = 0; u < U; ++u)
-                if (v + uint32_t(u) * nthr < d.v1) store_vec((RS_GLOBAL u32x4_u *)(dst + doff[u]), x[u]);
+            for (int u = 0; u < U; ++u) {
+                if (v + uint32_t(u) * nthr >= d.v1) continue;
+                if (!SHORT || w[u] >= 16u) store_vec((RS_GLOBAL u32x4_u *)(dst + doff[u]), x[u]);
+                else store_short(dst + doff[u], x[u], w[u]);
+            }
         }
     }
 }
@@ -1102,10 +1130,18 @@ __global__ __launch_bounds__(256) void reshard_gather_unit_kernel(KArgs<NPTR> ar
     const Desc d = load_desc(a, idx);
     stage_segments_u<NPTR, true>(d, a);
     __syncthreads();
+    if (d.ds[0] & kUShortSegs) {
+        switch (kind_levels(d.kind)) {
+            case 1: run_gather_unit<1, true>(d, a); break;
+            case 2: run_gather_unit<2, true>(d, a); break;
+            default: run_gather_unit<3, true>(d, a); break;
+        }
+        return;
+    }
     switch (kind_levels(d.kind)) {
-        case 1: run_gather_unit<1>(d, a); break;
-        case 2: run_gather_unit<2>(d, a); break;
-        default: run_gather_unit<3>(d, a); break;
+        case 1: run_gather_unit<1, false>(d, a); break;
+        case 2: run_gather_unit<2, false>(d, a); break;
+        default: run_gather_unit<3, false>(d, a); break;
     }
 }
 

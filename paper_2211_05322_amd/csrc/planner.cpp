@@ -918,17 +918,19 @@ bool lower_gather_unaligned(Plan &p, const std::vector<size_t> &group, int64_t c
         return false;
     }
     std::vector<Desc> mine;
-    // One receiver, segments of at least 16 bytes and under RS_UNIT_MAX_SEG
-    // on average: the unit gather (unaligned loads and stores, see desc.h).
+    // One receiver and segments under RS_UNIT_MAX_SEG bytes on average: the
+    // unit gather (unaligned loads and stores, see desc.h; a segment under
+    // 16 bytes is one unit moved byte by byte).
     // The slot form spends its time on slots that straddle two segments
     // (or rows), which short segments make frequent.  Measured against
     // destination slots: 8 % faster with 770-byte segments at fan-out 1;
     // slower at fan-out 2 and with rows of 6 KiB and more from one sender.
     bool unit = nfan <= int64_t(RS_UNIT_MAX_FAN) && row_bytes < int64_t(RS_UNIT_MAX_SEG) * int64_t(ns);
     uint32_t upr = 0;  // units per row
+    bool unit_short = false;
     for (size_t k = 0; k < ns; ++k) {
         const uint32_t w = (k + 1 < ns ? seg[k + 1].col : uint32_t(row_bytes)) - seg[k].col;
-        unit = unit && w >= 16;
+        unit_short = unit_short || w < 16;
         seg[k].pad = upr;
         upr += (w + 15) / 16;
     }
@@ -945,6 +947,7 @@ bool lower_gather_unaligned(Plan &p, const std::vector<size_t> &group, int64_t c
         }
         Desc u = d;
         u.kind = uint8_t(make_kind(4, uint32_t(levels)) | kUnitGather);
+        u.ds[0] = unit_short ? kUShortSegs : 0u;
         u.vpr = upr;
         const FastDiv fu = make_fastdiv(upr), fn = make_fastdiv(std::max<uint32_t>(1, upr / uint32_t(ns)));
         u.mul_vpr = fu.mul;

@@ -501,7 +501,8 @@ def test_unaligned_gather_declines():
 
 
 SHORT_SEGMENT_CASES = [
-    # segments under 16 bytes: slots of three or more pieces
+    # segments under 16 bytes: at fan-out 1 units of their own width, else
+    # slots of three or more pieces
     ((4, 8, 40), "float16", (8,), "RRS^0", (2,), "S^0RR"),              # 10-byte segments
     ((3, 16, 60), "uint8", (1, 8), "RRS^1", (2,), "RRR"),              # 8/7-byte segments, fan-out 2
     ((2, 12, 27), "float32", (1, 3, 3), "RRS^{12}", (1,), "RRR"),      # 12-byte segments
@@ -516,6 +517,13 @@ def test_host_unaligned_gather_short_segments(case, chunk):
     p = plan_of(*case, chunk_bytes=chunk)
     assert B.reshard_plan_unaligned_gather_chunks(p) > 0 and B.reshard_plan_realign_chunks(p) == 0
     host_case(*case, chunk_bytes=chunk)
+
+
+@pytest.mark.parametrize("case", SHORT_SEGMENT_CASES)
+def test_short_segments_take_units_at_fanout_one(case):
+    p = plan_of(*case)
+    fanout = B.reshard_plan_stats(p)["max_fanout"]
+    assert (B.reshard_plan_unit_gather_chunks(p) > 0) == (fanout == 1), fanout
 
 
 def test_gather_used_by_column_split_workloads():

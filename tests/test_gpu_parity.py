@@ -342,8 +342,9 @@ from tests.test_capi_host import SHORT_SEGMENT_CASES, UNALIGNED_GATHER_CASES  # 
 
 @pytest.mark.parametrize("case", SHORT_SEGMENT_CASES + [((4, 41, 77), "float16", (2, 2), "R S^0 S^1", (2,), "S^0 R R")])
 def test_unaligned_gather_short_segments_and_runs(case):
-    # segments under 16 bytes (slots of three or more pieces) and runs
-    # shorter than a chunk, on the unaligned row gather
+    # segments under 16 bytes (at fan-out 1 units of their own width, else
+    # slots of three or more pieces) and runs shorter than a chunk, on the
+    # unaligned row gather
     shape, dt, sm, ss, dm, ds = case
     _say(f"short segments / runs {case}")
     assert B.reshard_plan_unaligned_gather_chunks(B.reshard_plan(shape, dt, sm, ss, dm, ds)) > 0
