@@ -115,8 +115,10 @@ typedef struct {
                                from its fan-out (direct chunks: 16 waves per CU at fan-out
                                <= 2, 8 above; both row-gather kinds: 64 / fan-out waves, at
                                least 8, except unaligned row gathers with one sender per row,
-                               which take 32, 16 and 8 waves at fan-out 1, 2 and above; never
-                               below 2 workgroups); -1 = no cap */
+                               which take 32, 16 and 8 waves at fan-out 1, 2 and above, and
+                               32 at any fan-out when their chunks are under 3/4 full on
+                               average (rows in short runs); never below 2 workgroups);
+                               -1 = no cap */
     int32_t gather_band;    /* row-gather chunks: column segments per band (>= 0); the chunks
                                of a row group cover one band of the destination rows after
                                another; 0 = whole rows (default) */

@@ -1318,16 +1318,20 @@ reshard_status_t launch(const Plan &p, const Desc *descs, const int32_t *fan, co
     // per CU, as the aligned gather.  One sender per row (rows in runs, or
     // whole rows in another phase) reads like the direct kernel and wants
     // its caps: measured uncapped best at fan-out 1, 16 waves at 2 (10 %
-    // faster than uncapped), 8 at 4 (12 % faster than 16).
-    auto gather_u_lds = [&](int64_t fanout, int64_t segs) {
+    // faster than uncapped), 8 at 4 (12 % faster than 16) -- unless most
+    // chunks are cut short by their runs: each then makes one short pass,
+    // its latency is not hidden, and 32 waves are best (8 KiB runs at
+    // fan-out 4: 141 against 197 us).
+    auto gather_u_lds = [&](int64_t fanout, int64_t segs, bool short_chunks) {
         if (!p.tuning.cap_is_default) return user_lds;
         const uint32_t fan = uint32_t(fanout > 0 ? fanout : 1);
         uint32_t waves = 64u / fan > 8u ? 64u / fan : 8u;
-        if (segs == 1) waves = fan <= 1 ? 32u : fan == 2 ? 16u : 8u;
+        if (segs == 1) waves = fan <= 1 || short_chunks ? 32u : fan == 2 ? 16u : 8u;
         return residency_lds(waves, block < 256u ? block : 256u);
     };
     if (n_slot) {
-        const uint32_t ulds = gather_u_lds(p.gather_u_fanout, p.gather_u_segs);
+        const bool short_chunks = 4 * p.gather_u_bytes < 3 * p.gather_u_room;  // under 3/4 full
+        const uint32_t ulds = gather_u_lds(p.gather_u_fanout, p.gather_u_segs, short_chunks);
         a.descs = descs + n_direct + n_gather;
         const reshard_status_t st = launch_one(reshard_gather_u_kernel<NPTR>, a, n_slot, remap,
                                                block < 256u ? block : 256u,
@@ -1335,7 +1339,7 @@ reshard_status_t launch(const Plan &p, const Desc *descs, const int32_t *fan, co
         if (st != RESHARD_OK) return st;
     }
     if (n_unit) {
-        const uint32_t ulds = gather_u_lds(p.unit_fanout, p.unit_segs);
+        const uint32_t ulds = gather_u_lds(p.unit_fanout, p.unit_segs, false);
         a.descs = descs + n_direct + n_gather + n_slot;
         const reshard_status_t st = launch_one(reshard_gather_unit_kernel<NPTR>, a, n_unit, remap,
                                                block < 256u ? block : 256u, ulds > kUnitLds ? ulds : kUnitLds,

@@ -996,6 +996,8 @@ bool lower_gather_unaligned(Plan &p, const std::vector<size_t> &group, int64_t c
             d.ss[2] = uint32_t(base < rd0 ? rd0 - base : 0);
             d.src_rel0 = uint32_t(std::min<uint64_t>(16 * nsl, rd0 + run_bytes - base));
             mine.push_back(d);
+            p.gather_u_bytes += d.src_rel0 - d.ss[2];
+            p.gather_u_room += 16 * cv;
         }
     }
     p.segs.insert(p.segs.end(), seg.begin(), seg.end());
@@ -1034,6 +1036,8 @@ void lower(Plan &p) {
     p.gather_fanout = 0;
     p.gather_u_fanout = 0;
     p.gather_u_segs = 0;
+    p.gather_u_bytes = 0;
+    p.gather_u_room = 0;
     p.unit_fanout = 0;
     p.unit_segs = 0;
     std::vector<Desc> gdescs, udescs, unitdescs;
