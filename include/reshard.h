@@ -117,8 +117,9 @@ typedef struct {
                                least 8, except unaligned row gathers with one sender per row,
                                which take 32, 16 and 8 waves at fan-out 1, 2 and above, and
                                32 at any fan-out when their chunks are under 3/4 full on
-                               average (rows in short runs); never below 2 workgroups);
-                               -1 = no cap */
+                               average (rows in short runs); 32 for unaligned row gathers
+                               with segments under 16 bytes at fan-out up to 4; never below
+                               2 workgroups); -1 = no cap */
     int32_t gather_band;    /* row-gather chunks: column segments per band (>= 0); the chunks
                                of a row group cover one band of the destination rows after
                                another; 0 = whole rows (default) */

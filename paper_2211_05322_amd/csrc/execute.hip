@@ -1321,17 +1321,20 @@ reshard_status_t launch(const Plan &p, const Desc *descs, const int32_t *fan, co
     // faster than uncapped), 8 at 4 (12 % faster than 16) -- unless most
     // chunks are cut short by their runs: each then makes one short pass,
     // its latency is not hidden, and 32 waves are best (8 KiB runs at
-    // fan-out 4: 141 against 197 us).
-    auto gather_u_lds = [&](int64_t fanout, int64_t segs, bool short_chunks) {
+    // fan-out 4: 141 against 197 us).  Segments under 16 bytes (the slow
+    // slot path) want 32 waves too (fan-out 4: 382 against 390 us).
+    auto gather_u_lds = [&](int64_t fanout, int64_t segs, bool more_waves) {
         if (!p.tuning.cap_is_default) return user_lds;
         const uint32_t fan = uint32_t(fanout > 0 ? fanout : 1);
         uint32_t waves = 64u / fan > 8u ? 64u / fan : 8u;
-        if (segs == 1) waves = fan <= 1 || short_chunks ? 32u : fan == 2 ? 16u : 8u;
+        if (segs == 1) waves = fan <= 1 ? 32u : fan == 2 ? 16u : 8u;
+        if (more_waves && waves < 32u) waves = 32u;
         return residency_lds(waves, block < 256u ? block : 256u);
     };
     if (n_slot) {
-        const bool short_chunks = 4 * p.gather_u_bytes < 3 * p.gather_u_room;  // under 3/4 full
-        const uint32_t ulds = gather_u_lds(p.gather_u_fanout, p.gather_u_segs, short_chunks);
+        const bool short_chunks = p.gather_u_segs == 1 && 4 * p.gather_u_bytes < 3 * p.gather_u_room;
+        const bool short_segs = p.gather_u_short && p.gather_u_fanout <= 4;  // measured up to fan-out 4
+        const uint32_t ulds = gather_u_lds(p.gather_u_fanout, p.gather_u_segs, short_chunks || short_segs);
         a.descs = descs + n_direct + n_gather;
         const reshard_status_t st = launch_one(reshard_gather_u_kernel<NPTR>, a, n_slot, remap,
                                                block < 256u ? block : 256u,

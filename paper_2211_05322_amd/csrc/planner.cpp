@@ -1010,6 +1010,7 @@ bool lower_gather_unaligned(Plan &p, const std::vector<size_t> &group, int64_t c
     } else {
         p.gather_u_fanout = std::max(p.gather_u_fanout, nfan);
         p.gather_u_segs = std::max(p.gather_u_segs, int64_t(ns));
+        p.gather_u_short = p.gather_u_short || (d.ds[0] & kUShortSegs) != 0;
     }
     return true;
 }
@@ -1038,6 +1039,7 @@ void lower(Plan &p) {
     p.gather_u_segs = 0;
     p.gather_u_bytes = 0;
     p.gather_u_room = 0;
+    p.gather_u_short = false;
     p.unit_fanout = 0;
     p.unit_segs = 0;
     std::vector<Desc> gdescs, udescs, unitdescs;

@@ -90,6 +90,7 @@ struct Plan {
     int64_t gather_u_segs = 0;   // most segments per row among unaligned row-gather groups
     uint64_t gather_u_bytes = 0; // destination bytes of the slot chunks, and their nominal
     uint64_t gather_u_room = 0;  //     capacity (chunks x chunk size): how full they are
+    bool gather_u_short = false; // some slot group has segments under 16 bytes
     int64_t unit_fanout = 0;     // ... and among the unit-gather groups:
     int64_t unit_segs = 0;       //     receivers, segments per row
     int64_t direct_fanout = 0; // largest receiver count among direct chunks
