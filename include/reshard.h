@@ -279,6 +279,9 @@ reshard_status_t reshard_plan_stats(const reshard_plan_t *plan, int64_t *bytes_r
                                     int64_t *bytes_written, int64_t *n_unit_tasks,
                                     int64_t *n_descriptors, int64_t *max_fanout);
 
+/* Introspection of the lowering, the chunks each unit task's broadcast is
+ * cut into (Section 3.1): plan properties and chunk counts per kind. */
+
 /* Required byte alignment of every buffer pointer passed to reshard_execute
  * (1..16), or 0 for a NULL plan. */
 int64_t reshard_plan_alignment(const reshard_plan_t *plan);
@@ -297,17 +300,17 @@ int64_t reshard_plan_realign_chunks(const reshard_plan_t *plan);
  * (RESHARD_NO_GATHER turns them off), or -1 for a NULL plan. */
 int64_t reshard_plan_gather_chunks(const reshard_plan_t *plan);
 
-/* Number of workgroup chunks that write 16-byte slots of destination rows
- * (contiguous, or contiguous in runs of at least one chunk) gathered from
- * senders whose row segments have any widths of at least 16 bytes and any
- * byte alignment (uneven splits, rows in different 16-byte phases;
- * RESHARD_NO_GATHER turns them off), or -1 for a NULL plan. */
+/* Number of workgroup chunks that write destination rows (contiguous, or
+ * contiguous in runs of at least 2 KiB) gathered from senders whose row
+ * segments have any widths and any byte alignment (uneven splits, rows in
+ * different 16-byte phases; RESHARD_NO_GATHER turns them off), or -1 for a
+ * NULL plan. */
 int64_t reshard_plan_unaligned_gather_chunks(const reshard_plan_t *plan);
 
 /* Of reshard_plan_unaligned_gather_chunks, the number that move 16-byte
- * units of each segment with unaligned loads and stores (one or two
- * receivers, every segment at least 16 bytes; a kernel of their own), or -1
- * for a NULL plan. */
+ * units of each segment with unaligned loads and stores (one receiver,
+ * segments under 2 KiB on average; a kernel of their own), or -1 for a NULL
+ * plan. */
 int64_t reshard_plan_unit_gather_chunks(const reshard_plan_t *plan);
 
 /* Number of workgroup chunks that transpose tiles through LDS (tasks whose
