@@ -768,11 +768,11 @@ bool lower_gather_group(Plan &p, const std::vector<size_t> &group, int64_t chunk
 #define RS_UNIT_MAX_SEG 2048  // the unit gather takes mean segment widths below this (bytes)
 #endif
 
-// Unaligned row gather of one group (see desc.h): segments of any widths of
-// at least 16 bytes tiling the destination row (one segment per row too,
-// when its rows are in different 16-byte phases on the two sides),
-// destination rows contiguous.  Returns false, emitting nothing, when the
-// group does not qualify.
+// Unaligned row gather of one group (see desc.h): segments of any widths
+// tiling the destination row (one segment per row too, when its rows are in
+// different 16-byte phases on the two sides), destination rows contiguous
+// whole or in runs.  Returns false, emitting nothing, when the group does
+// not qualify.
 bool lower_gather_unaligned(Plan &p, const std::vector<size_t> &group, int64_t chunk_bytes, std::vector<Desc> &out,
                             std::vector<Desc> &unit_out) {
     const int nd = p.ndim;
