@@ -573,7 +573,9 @@ __global__ __launch_bounds__(1024) void reshard_gather_kernel(KArgs<NPTR> args) 
 // LDS: 64-bit source pointers at 0, three strides per segment at
 // 8 * kMaxSegs, segment starts (bytes within the row) at 20 * kMaxSegs.
 constexpr uint32_t kGatherULds = 24u * kMaxSegs;
-constexpr uint32_t kUnitLds = 28u * kMaxSegs;  // the same + first units at 24 * kMaxSegs
+// the same + first units at 24 * kMaxSegs, the short segments' indices at
+// 28 * kMaxSegs and their count at 32 * kMaxSegs
+constexpr uint32_t kUnitLds = 32u * kMaxSegs + 16u;
 
 // Chunk order of the unaligned row gather: the dispatcher hands workgroups to
 // the 8 XCDs in turn, so blocks b, b + 8, ..., b + 8 (kUGroup - 1) share an
@@ -601,7 +603,15 @@ __device__ __forceinline__ void stage_segments_u(const Desc &d, const RS_CONST K
         sst[3 * g + 1] = segs[g].ss[1];
         sst[3 * g + 2] = segs[g].ss[2];
         scol[g] = segs[g].col;
-        if (UNITS) reinterpret_cast<uint32_t *>(rs_lds + 24u * kMaxSegs)[g] = segs[g].pad;
+        if (UNITS) {
+            reinterpret_cast<uint32_t *>(rs_lds + 24u * kMaxSegs)[g] = segs[g].pad;
+            // segments under 16 bytes, listed in any order (the count was
+            // cleared before the barrier that precedes this staging)
+            if ((d.ds[0] & kUShortSegs) && (g + 1 < d.pad[1] ? segs[g + 1].col : d.run) - segs[g].col < 16u) {
+                const uint32_t k = atomicAdd(reinterpret_cast<uint32_t *>(rs_lds + 32u * kMaxSegs), 1u);
+                reinterpret_cast<uint32_t *>(rs_lds + 28u * kMaxSegs)[k] = g;
+            }
+        }
     }
 }
 
@@ -869,8 +879,10 @@ __device__ __forceinline__ void store_short(RS_GLOBAL unsigned char *q, u32x4 v,
         if (i < n) q[i] = (unsigned char)(x[i >> 2] >> (8u * (i & 3u)));
 }
 
-// SHORT: the group has segments shorter than 16 bytes (each one unit, moved
-// by load_short / store_short).
+// SHORT: the group has segments shorter than 16 bytes.  Each is one unit,
+// skipped by the main loop and moved afterwards in one pass over the
+// chunk's short units (load_short / store_short), so the waves of the main
+// loop never branch to the byte path.
 template <int L, bool SHORT, int NPTR>
 __device__ __forceinline__ void run_gather_unit(const Desc &d, const RS_CONST KArgs<NPTR> *a) {
     constexpr int U = RS_UNIT_U;  // units per lane per pass, loads first
@@ -890,17 +902,37 @@ __device__ __forceinline__ void run_gather_unit(const Desc &d, const RS_CONST KA
                 const RS_GLOBAL unsigned char *src;
                 unit_addr<L, U>(d, sp, sst, scol, sunit, vu, src, doff[u], w[u]);
                 if (!SHORT || w[u] >= 16u) x[u] = *(const RS_GLOBAL u32x4_u *)src;
-                else x[u] = load_short(src, w[u]);
             }
         }
         for (uint32_t r = 0; r < d.nfan; ++r) {
             RS_GLOBAL unsigned char *dst = (RS_GLOBAL unsigned char *)a->ptr[a->nsrc + uint32_t(fan[r])] + d.dst_base;
 #pragma unroll
             for (int u = 0; u < U; ++u) {
-                if (v + uint32_t(u) * nthr >= d.v1) continue;
-                if (!SHORT || w[u] >= 16u) store_vec((RS_GLOBAL u32x4_u *)(dst + doff[u]), x[u]);
-                else store_short(dst + doff[u], x[u], w[u]);
+                if (v + uint32_t(u) * nthr >= d.v1 || (SHORT && w[u] < 16u)) continue;
+                store_vec((RS_GLOBAL u32x4_u *)(dst + doff[u]), x[u]);
             }
+        }
+    }
+    if constexpr (SHORT) {
+        // the chunk's short units: (row, short segment) pairs of its rows
+        const uint32_t *sshort = reinterpret_cast<const uint32_t *>(rs_lds + 28u * kMaxSegs);
+        const uint32_t nsh = *reinterpret_cast<const uint32_t *>(rs_lds + 32u * kMaxSegs);
+        const uint32_t ns = d.pad[1], rb = d.run;
+        const uint32_t r0 = fastdiv(d.v0, d.mul_vpr, d.sh_vpr), r1 = fastdiv(d.v1 - 1u, d.mul_vpr, d.sh_vpr);
+        const uint32_t total = (r1 - r0 + 1u) * nsh;
+        for (uint32_t i = threadIdx.x; i < total; i += nthr) {
+            const uint32_t rr = i / nsh, g = sshort[i - rr * nsh], r = r0 + rr;
+            const uint32_t vu = r * d.vpr + sunit[g];
+            if (vu < d.v0 || vu >= d.v1) continue;
+            const uint32_t ws = (g + 1 < ns ? scol[g + 1] : rb) - scol[g];
+            uint32_t i1, i2, i3;
+            row_indices<L>(d, d.ss[0] + r, i1, i2, i3);
+            const RS_GLOBAL unsigned char *q =
+                (const RS_GLOBAL unsigned char *)(sp[g] + (i1 * sst[3 * g] + i2 * sst[3 * g + 1] + i3 * sst[3 * g + 2]));
+            const u32x4 y = load_short(q, ws);
+            const uint32_t off = (r - d.ss[1]) * rb + scol[g];
+            for (uint32_t k = 0; k < d.nfan; ++k)
+                store_short((RS_GLOBAL unsigned char *)a->ptr[a->nsrc + uint32_t(fan[k])] + d.dst_base + off, y, ws);
         }
     }
 }
@@ -1136,6 +1168,10 @@ __global__ __launch_bounds__(256) void reshard_gather_unit_kernel(KArgs<NPTR> ar
     const uint32_t idx = a->per_xcd ? (b & 7u) * a->per_xcd + (b >> 3) : grouped_chunk(b);
     if (idx >= a->ndesc) return;
     const Desc d = load_desc(a, idx);
+    if (d.ds[0] & kUShortSegs) {  // uniform: clear the short-segment count first
+        if (threadIdx.x == 0) *reinterpret_cast<uint32_t *>(rs_lds + 32u * kMaxSegs) = 0u;
+        __syncthreads();
+    }
     stage_segments_u<NPTR, true>(d, a);
     __syncthreads();
     if (d.ds[0] & kUShortSegs) {
