@@ -2,7 +2,9 @@
 
 GPU: its output equals reshard_execute's, bit for bit, on calls in a row
 through the C ABI -- workload 5 at full size (the largest table of the
-workloads), then smaller inputs of other kernel kinds, then the first plan
+workloads), then smaller inputs of every other kernel kind that reads the
+tables (slots and units of the unaligned row gather, direct chunks, tile
+transposes), then the first plan
 again on the same stream with new source data (the tables it left in the
 scratch are reused) -- and the oracle's on the small inputs.  CPU: a plan
 whose tables exceed the scratch is refused before any HIP call.
@@ -85,32 +87,41 @@ def test_noalloc_equals_execute_on_calls_in_a_row():
     _same(a, b, "workload 5")
     del a, b
 
-    # calls 2 and 3: smaller inputs, other kernel kinds (unaligned row
-    # gather; direct chunks), also checked against the oracle
-    for shape, w, label in (((2, 64, 390), w5, "unaligned row gather"),
-                            ((4, 8, 66, 16), WORKLOADS[4], "direct")):
+    # calls 2 to 5: smaller inputs, other kernel kinds (unaligned row gather
+    # over slots and over units, direct chunks, tile transposes), also
+    # checked against the oracle
+    one_rep = ((1, 8), "R S^1 R")
+    for shape, w, dst, perm, label in (((2, 64, 390), w5, None, None, "unaligned row gather"),
+                                       ((2, 64, 390), w5, one_rep, None, "unit gather"),
+                                       ((4, 8, 66, 16), WORKLOADS[4], None, None, "direct"),
+                                       ((2, 64, 1024), w5, None, (0, 2, 1), "tile transpose")):
         _say(f"noalloc smaller call: {label} {shape}")
+        dm, ds = dst or (w.dst_mesh, w.dst_spec)
         xs = make_tensor(shape, w.dtype, "normal", seed=1)
         xb = as_numpy_bits(xs)
         want = oracle.reshard(oracle.shard(xb, w.src_mesh, w.src_spec), shape, w.src_mesh, w.src_spec,
-                              w.dst_mesh, w.dst_spec)
-        p = B.reshard_plan(shape, w.dtype, w.src_mesh, w.src_spec, w.dst_mesh, w.dst_spec)
+                              dm, ds, dst_perm=perm)
+        p = B.reshard_plan(shape, w.dtype, w.src_mesh, w.src_spec, dm, ds, dst_perm=perm)
+        kind = {"unit gather": B.reshard_plan_unit_gather_chunks,
+                "tile transpose": B.reshard_plan_transpose_chunks}.get(label)
+        assert kind is None or kind(p) > 0, label
         sd = _scatter(w, shape, xs.cuda())
         a, b = _both(p, sd, stream)
         _same(a, b, label)
         for k, (t, ref) in enumerate(zip(b, want)):
-            assert np.array_equal(as_numpy_bits(t), ref), f"{label}: destination {k} differs from the oracle"
+            got = as_numpy_bits(t).reshape(ref.shape)
+            assert np.array_equal(got, ref), f"{label}: destination {k} differs from the oracle"
 
-    # call 4: the first plan again on the same stream after another plan
+    # call 6: the first plan again on the same stream after another plan
     # took the scratch, new source data
-    _say("noalloc call 4: workload 5 again, new data")
+    _say("noalloc call 6: workload 5 again, new data")
     x2 = make_workload_tensor(w5, seed=7, device="cuda")
     src2 = _scatter(w5, w5.shape, x2)
     a, b = _both(big, src2, stream)
     _same(a, b, "workload 5 again")
 
-    # call 5: the same plan on the same stream right after (tables reused)
-    _say("noalloc call 5: workload 5, tables in place")
+    # call 7: the same plan on the same stream right after (tables reused)
+    _say("noalloc call 7: workload 5, tables in place")
     b2 = B.empty_shards(big, 1)
     B.reshard_execute_noalloc(big, src2, b2, stream=stream)
     torch.cuda.synchronize()
