@@ -202,7 +202,9 @@ constexpr TileAt tile_offsets(const Desc &d, uint32_t t, uint32_t es) {
 // LDS byte offset of byte `o` of 16-byte column slot c in tile row r: rows
 // are kTileBytes apart, and the slot is XOR-swizzled by the row's group of
 // 16 / es rows, so the column reads of the store phase (16 / es rows of one
-// slot per output vector, 8 output vectors per wave) hit distinct banks.
+// slot per output vector) of a 128-byte-wide tile hit distinct banks.  In
+// wider tiles 32 lanes read one column through 8 slots and conflict; a
+// conflict-free lane order measured no faster (the kernel is not LDS-bound).
 constexpr uint32_t tile_lds(uint32_t r, uint32_t c, uint32_t o, uint32_t es) {
     return r * kTileBytes + ((c ^ ((r / (16u / es)) & 7u)) << 4) + o;
 }
