@@ -7,7 +7,8 @@ arithmetic with every access bounds-checked) against the oracle, bit for
 bit, on seeded cases that span several tiles with ragged edges, every
 element size, aligned and unaligned rows, and on argument errors.  GPU: the
 kernels against the oracle on the same kinds of cases and on a transposed
-activation at full size, every destination element compared.
+activations at full size, every destination element compared, and seeded
+permuted cases under random launch tunings.
 """
 
 import random
@@ -182,15 +183,35 @@ def test_gpu_transpose_unaligned_rows():
         _gpu_run(shape, "float16", (1,), "R" * len(shape), None, (2,), "S^0" + "R" * (len(shape) - 1), dp)
 
 
+def _tunings(n, seed):
+    rng = random.Random(seed)
+    return [{k: v for k, v in (("chunk_bytes", rng.choice([0, 64, 1000, 8192, 40000])),
+                               ("block_threads", rng.choice([0, 64, 128, 256, 512])),
+                               ("max_wgs_per_cu", rng.choice([0, 2, 4, -1]))) if v} for _ in range(n)]
+
+
 @pytest.mark.gpu
-def test_gpu_transposed_activation_full_size():
-    # the GPT activation fp16 [8, 1024, 4096] from (2,4) S^0 R S^1 to (2,4)
-    # R S^0 S^1 with the destination in [batch, hidden, seq] order: every
-    # destination element compared with the tensor transposed at the
-    # oracle's boxes, on the GPU
+@pytest.mark.parametrize("case,tuning", list(zip(perm_cases(120, 91), _tunings(120, 92))))
+def test_gpu_permuted_fuzz_tunings(case, tuning):
+    # seeded permuted layouts under random chunk sizes, workgroup sizes and
+    # residency caps (the tile transpose, and the direct and gather chunks
+    # of permuted plans, under every launch shape)
+    shape, dt, sm, ss, sp, dm, ds, dp, _ = case
+    print(f"permuted fuzz {case} {tuning}", flush=True)
+    _gpu_run(shape, dt, sm, ss, sp, dm, ds, dp, **tuning)
+
+
+@pytest.mark.gpu
+@pytest.mark.parametrize("name", ["transposed2", "transposed5"])
+def test_gpu_transposed_activation_full_size(name):
+    # the GPT activations fp16 [8, 1024, 4096] (2,4) S^0 R S^1 -> (2,4)
+    # R S^0 S^1 and fp16 [8, 2048, 12288] (4,8) R R S^{01} -> (4,8) R S^1 R
+    # (4 replicas) with the destination in [batch, hidden, seq] order, in the
+    # benchmark's launch configuration: every destination element compared
+    # with the tensor transposed at the oracle's boxes, on the GPU
     import torch
     from paper_2211_05322_amd.workloads import make_tensor, workload_by_name
-    w = workload_by_name("transposed2")
+    w = workload_by_name(name)
     print(f"transposed activation {w.shape}", flush=True)
     x = make_tensor(w.shape, w.dtype, "normal", seed=0).cuda()
     n = len(w.shape)
