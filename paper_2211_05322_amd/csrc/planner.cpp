@@ -923,8 +923,9 @@ bool lower_gather_unaligned(Plan &p, const std::vector<size_t> &group, int64_t c
     // 16 bytes is one unit moved byte by byte).
     // The slot form spends its time on slots that straddle two segments
     // (or rows), which short segments make frequent.  Measured against
-    // destination slots: 8 % faster with 770-byte segments at fan-out 1;
-    // slower at fan-out 2 and with rows of 6 KiB and more from one sender.
+    // destination slots: 8 % faster with 770-byte segments at fan-out 1, 18 %
+    // with 4-byte segments among them; slower at fan-out 2 and with rows of
+    // 6 KiB and more from one sender.
     bool unit = nfan <= int64_t(RS_UNIT_MAX_FAN) && row_bytes < int64_t(RS_UNIT_MAX_SEG) * int64_t(ns);
     uint32_t upr = 0;  // units per row
     bool unit_short = false;
