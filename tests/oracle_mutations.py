@@ -133,6 +133,38 @@ def _shard_inverse_perm(x, mesh, spec, perm=None):
     return _SHARD(x, mesh, spec, perm)
 
 
+def _shard_perm_reshape(x, mesh, spec, perm=None):
+    # the buffer reshaped to the permuted extents instead of transposed
+    plain = _SHARD(x, mesh, spec)
+    if perm is None:
+        return plain
+    perm = R.check_perm(perm, x.ndim)
+    return [np.ascontiguousarray(a.reshape(tuple(a.shape[k] for k in perm))) for a in plain]
+
+
+_UNSHARD = R.unshard
+
+
+def _unshard_perm_reshape(shards, shape, mesh, spec, perm=None):
+    # permuted buffers reshaped back to the box instead of transposed
+    if perm is None:
+        return _UNSHARD(shards, shape, mesh, spec)
+    dims = R.parse_spec(spec, len(shape), len(mesh))
+    plain = []
+    for d, s in enumerate(shards):
+        box = R.device_box(tuple(shape), mesh, dims, d)
+        plain.append(np.asarray(s).reshape(tuple(hi - lo for lo, hi in box)))
+    return _UNSHARD(plain, shape, mesh, spec)
+
+
+_LOCAL_SHAPE = R.local_shape
+
+
+def _local_shape_unpermuted(shape, mesh, spec, device, perm=None):
+    # the box's extents in tensor order whatever the buffer's order
+    return _LOCAL_SHAPE(shape, mesh, spec, device)
+
+
 # scheduling across hosts (Section 3.2)
 
 def _start_times_sender_only(model, order, host):
@@ -236,6 +268,9 @@ MUTATIONS = {
     "unshard_without_replica_check": (R, "unshard", _unshard_without_replica_check, _PINS_R),
     "traffic_unique_writes": (R, "traffic_bytes", _traffic_unique_writes, _PINS_R),
     "shard_inverse_perm": (R, "shard", _shard_inverse_perm, _PINS_R),
+    "shard_perm_reshape": (R, "shard", _shard_perm_reshape, _PINS_R),
+    "unshard_perm_reshape": (R, "unshard", _unshard_perm_reshape, _PINS_R),
+    "local_shape_unpermuted": (R, "local_shape", _local_shape_unpermuted, _PINS_R),
     "parse_spec_first_axis_only": (R, "parse_spec", _parse_spec_first_axis_only, _PINS_R),
     "parse_spec_axes_reversed": (R, "parse_spec", _parse_spec_axes_reversed, _PINS_R),
     "start_times_sender_only": (SCH, "start_times", _start_times_sender_only, _PINS_S),
