@@ -181,6 +181,11 @@ reshard_status_t make_plan(int ndim, const int64_t *shape, reshard_dtype_t dtype
             delete p;
             return fail(RESHARD_EUNSUPPORTED, "lowering needs more than 2^24 workgroup chunks");
         }
+        if (p->tile_span_too_long) {
+            delete p;
+            return fail(RESHARD_EUNSUPPORTED,
+                        "a transpose tile of the permuted layouts would span 2^32 bytes or more of one buffer");
+        }
     } catch (const std::bad_alloc &) {
         delete p;
         return fail(RESHARD_ENOMEM, "out of host memory while planning");

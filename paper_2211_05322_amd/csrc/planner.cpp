@@ -482,7 +482,7 @@ struct TPiece {
 
 void emit_transpose(Plan &p, const TPiece &tp, int32_t src_buf, int64_t fan_off, int64_t nfan, int64_t chunk_bytes,
                     std::vector<Desc> &out) {
-    if (p.too_many) return;
+    if (p.too_many || p.tile_span_too_long) return;
     if (tp.outer.size() > 2) {
         const Level top = tp.outer.front();
         TPiece sub = tp;
@@ -516,15 +516,39 @@ void emit_transpose(Plan &p, const TPiece &tp, int32_t src_buf, int64_t fan_off,
                     sub.dst_off = tp.dst_off + uint64_t(i * top.ds);
                     emit_transpose(p, sub, src_buf, fan_off, nfan, chunk_bytes, out);
                 }
-            } else {
-                const int64_t half = std::max<int64_t>(4 * te, (tp.nb / 2) / (4 * te) * (4 * te));
-                for (int64_t b0 = 0; b0 < tp.nb; b0 += half) {
-                    TPiece sub = tp;
-                    sub.nb = std::min(half, tp.nb - b0);
-                    sub.src_off = tp.src_off + uint64_t(b0 * tp.ss_b);
-                    sub.dst_off = tp.dst_off + uint64_t(b0 * es);
-                    emit_transpose(p, sub, src_buf, fan_off, nfan, chunk_bytes, out);
+                return;
+            }
+            // A and B only: the source span grows with B (stride ss_b) and
+            // with A's run, the destination span with A (stride ds_a) and
+            // with B's run.  Halve the extent behind the larger term of the
+            // span that is too long, in whole tiles (whole 4-tile groups
+            // along B while it is long).
+            const uint64_t sb_term = uint64_t(tp.nb - 1) * uint64_t(tp.ss_b), sa_term = uint64_t(tp.na * es);
+            const uint64_t da_term = uint64_t(tp.na - 1) * uint64_t(tp.ds_a), db_term = uint64_t(tp.nb * es);
+            const bool cut_b = ss_ >= kMaxChunkSpan ? sb_term >= sa_term : db_term > da_term;
+            const int64_t n = cut_b ? tp.nb : tp.na;
+            // One tile along that extent already too long: the caller admits
+            // only pieces whose tile strides fit 31 bits, so this cannot
+            // happen there; it fails the plan rather than recursing forever.
+            if (n <= te) {
+                p.tile_span_too_long = true;
+                return;
+            }
+            const int64_t step = n / 2 >= 4 * te && cut_b ? 4 * te : te;
+            const int64_t half = std::max<int64_t>(step, (n / 2) / step * step);
+            for (int64_t x0 = 0; x0 < n; x0 += half) {
+                TPiece sub = tp;
+                if (cut_b) {
+                    sub.nb = std::min(half, tp.nb - x0);
+                    sub.src_off = tp.src_off + uint64_t(x0 * tp.ss_b);
+                    sub.dst_off = tp.dst_off + uint64_t(x0 * es);
+                } else {
+                    sub.na = std::min(half, tp.na - x0);
+                    sub.src_off = tp.src_off + uint64_t(x0 * es);
+                    sub.dst_off = tp.dst_off + uint64_t(x0 * tp.ds_a);
                 }
+                emit_transpose(p, sub, src_buf, fan_off, nfan, chunk_bytes, out);
+                if (p.too_many || p.tile_span_too_long) return;
             }
             return;
         }
@@ -1027,6 +1051,7 @@ void lower(Plan &p) {
     p.lds_bytes = 0;
     p.transpose_rows = 0;
     p.too_many = false;
+    p.tile_span_too_long = false;
     p.max_fanout = 0;
     p.bytes_read = 0;
     for (const auto &t : p.tasks) p.bytes_read += t.bytes;

@@ -76,6 +76,7 @@ struct Plan {
     int64_t bytes_read = 0, bytes_written = 0, max_fanout = 0;
     int64_t align = 1;         // required buffer alignment in bytes
     bool too_many = false;     // lowering stopped: descriptor table over its cap
+    bool tile_span_too_long = false;  // lowering stopped: one transpose tile spans 2^32 bytes or more
     uint32_t lds_bytes = 0;    // LDS the realignment chunks need per workgroup
     size_t n_direct = 0;       // descs[0, n_direct): direct chunks
     size_t n_gather = 0;       // descs[n_direct, n_direct + n_gather): row-gather chunks;

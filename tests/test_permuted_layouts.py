@@ -130,6 +130,29 @@ def test_permutation_errors():
     assert e.value.status == B.RESHARD_EUNSUPPORTED
 
 
+# buffers above 4 GiB: a transpose piece must keep every tile within 32-bit
+# offsets of its origin, cut along A or B (whichever stride makes the span
+# too long) -- planning only here, the GPU tests below run them
+BIG_TRANSPOSES = [((1, 70000, 70000), "uint8", None, (0, 2, 1)),
+                  ((1, 40000, 60000), "float16", (0, 2, 1), None)]
+
+
+@pytest.mark.parametrize("shape,dt,sp,dp", BIG_TRANSPOSES)
+def test_transpose_pieces_above_4_gib_plan(shape, dt, sp, dp):
+    p = B.reshard_plan(shape, dt, (1,), "RRR", (1,), "RRR", src_perm=sp, dst_perm=dp)
+    assert B.reshard_plan_transpose_chunks(p) > 0
+    assert B.reshard_plan_stats(p)["n_descriptors"] == B.reshard_plan_transpose_chunks(p)
+
+
+def test_tile_strides_beyond_31_bits_take_the_element_path():
+    # 128 destination rows of one tile would lie 34 MB apart: the planner
+    # keeps such layouts off the transpose kernel (plain element pieces)
+    p = B.reshard_plan((1, 200, 34000000), "uint8", (1,), "RRR", (1,), "RRR", src_perm=(0, 2, 1))
+    assert B.reshard_plan_transpose_chunks(p) == 0
+    st = B.reshard_plan_stats(p)
+    assert st["bytes_written"] == 200 * 34000000 and st["n_descriptors"] > 0
+
+
 # --------------------------------------------------------------------- GPU
 
 def _gpu_run(shape, dt, sm, ss, sp, dm, ds, dp, seed=0, **kw):
@@ -230,3 +253,23 @@ def test_gpu_transposed_activation_full_size(name):
         box = oracle.device_box(w.shape, w.dst_mesh, dims, k)
         ref = xb[tuple(slice(lo, hi) for lo, hi in box)].permute(*w.dst_perm)
         assert torch.equal(t.view(torch.int16), ref), f"destination {k}"
+
+
+@pytest.mark.gpu
+@pytest.mark.parametrize("shape,dt,sp,dp", BIG_TRANSPOSES)
+def test_gpu_transpose_above_4_gib(shape, dt, sp, dp):
+    # every byte of a transposed buffer above 4 GiB against torch's permute
+    import torch
+    print(f"transpose above 4 GiB {shape} {dt} src_perm={sp} dst_perm={dp}", flush=True)
+    bits = torch.uint8 if dt == "uint8" else torch.int16
+    lo, hi = (0, 256) if dt == "uint8" else (-32768, 32768)
+    g = torch.Generator(device="cuda").manual_seed(5)
+    x = torch.randint(lo, hi, shape, dtype=bits, device="cuda", generator=g)
+    src = x.permute(*sp).contiguous() if sp else x
+    p = B.reshard_plan(shape, dt, (1,), "RRR", (1,), "RRR", src_perm=sp, dst_perm=dp)
+    dst = B.empty_shards(p, 1)
+    assert dst[0].numel() * dst[0].element_size() > (4 << 30)
+    B.reshard_execute(p, [src], dst)
+    torch.cuda.synchronize()
+    ref = x.permute(*dp) if dp else x
+    assert torch.equal(dst[0].view(bits), ref)
