@@ -270,6 +270,20 @@ bool monotone(const Piece &pc) {
     return true;
 }
 
+// Whether the chunks of a piece (from 0 to n, each ending where next_end
+// says) fit in the descriptor budget.  Counts without building any, so a
+// piece cut into too many chunks fails before it takes memory.
+template <class F>
+bool fits_chunk_budget(Plan &p, uint64_t n, F next_end) {
+    uint64_t k = p.descs.size();
+    for (uint64_t x = 0; x < n; x = next_end(x))
+        if (++k > kMaxDescs) {
+            p.too_many = true;
+            return false;
+        }
+    return true;
+}
+
 // Realignment path: chunks are ranges of whole rows.
 void emit_realign(Plan &p, const Piece &pc, int32_t src_buf, int64_t fan_off, int64_t nfan, int64_t chunk_bytes) {
     Desc d{};
@@ -302,16 +316,26 @@ void emit_realign(Plan &p, const Piece &pc, int32_t src_buf, int64_t fan_off, in
         return;
     }
     const bool mono = monotone(pc);
-    for (uint64_t r0 = 0; r0 < rows;) {
+    // end of the chunk from row r0: cr rows, fewer where they would span
+    // 2^31 bytes (the kernel forms signed 32-bit word offsets)
+    auto chunk_end = [&](uint64_t r0, const std::pair<uint64_t, uint64_t> &first) {
         uint64_t r1 = std::min(rows, r0 + cr);
-        const auto first = mono ? piece_off64(pc, 1, r0) : std::pair<uint64_t, uint64_t>(pc.src_off, pc.dst_off);
-        for (; mono;) {  // spans below 2^31: the kernel forms signed 32-bit word offsets
+        for (; mono;) {
             const auto last = piece_off64(pc, 1, r1 - 1);
             if (last.first + uint64_t(pc.run) - first.first < kMaxChunkSpan / 2 &&
                 last.second + uint64_t(pc.run) - first.second < kMaxChunkSpan / 2)
                 break;
             r1 = r0 + (r1 - r0) / 2;
         }
+        return r1;
+    };
+    if (mono && p.descs.size() + rows > kMaxDescs && !fits_chunk_budget(p, rows, [&](uint64_t r0) {
+            return chunk_end(r0, piece_off64(pc, 1, r0));
+        }))
+        return;
+    for (uint64_t r0 = 0; r0 < rows;) {
+        const auto first = mono ? piece_off64(pc, 1, r0) : std::pair<uint64_t, uint64_t>(pc.src_off, pc.dst_off);
+        const uint64_t r1 = chunk_end(r0, first);
         if (p.descs.size() >= kMaxDescs) {
             p.too_many = true;
             return;
@@ -371,16 +395,26 @@ void emit(Plan &p, const Piece &pc, int32_t src_buf, int64_t fan_off, int64_t nf
         return;
     }
     const bool mono = monotone(pc);
-    for (uint64_t v0 = 0; v0 < total;) {
+    // end of the chunk from vector v0: cv vectors, fewer where they would
+    // span 2^32 bytes on either side
+    auto chunk_end = [&](uint64_t v0, const std::pair<uint64_t, uint64_t> &first) {
         uint64_t v1 = std::min(total, v0 + cv);
-        const auto first = mono ? piece_off64(pc, vpr, v0) : std::pair<uint64_t, uint64_t>(pc.src_off, pc.dst_off);
-        for (; mono;) {  // shrink until the chunk spans < 2^32 bytes on both sides
+        for (; mono;) {
             const auto last = piece_off64(pc, vpr, v1 - 1);
             if (last.first + uint64_t(pc.w) - first.first < kMaxChunkSpan &&
                 last.second + uint64_t(pc.w) - first.second < kMaxChunkSpan)
                 break;
             v1 = v0 + (v1 - v0) / 2;
         }
+        return v1;
+    };
+    if (mono && p.descs.size() + total > kMaxDescs && !fits_chunk_budget(p, total, [&](uint64_t v0) {
+            return chunk_end(v0, piece_off64(pc, vpr, v0));
+        }))
+        return;
+    for (uint64_t v0 = 0; v0 < total;) {
+        const auto first = mono ? piece_off64(pc, vpr, v0) : std::pair<uint64_t, uint64_t>(pc.src_off, pc.dst_off);
+        const uint64_t v1 = chunk_end(v0, first);
         if (p.descs.size() >= kMaxDescs) {
             p.too_many = true;
             return;
@@ -408,6 +442,7 @@ void peel_top(Plan &p, const Piece &pc, int32_t src_buf, int64_t fan_off, int64_
         sub.src_off = pc.src_off + uint64_t(i * top.ss);
         sub.dst_off = pc.dst_off + uint64_t(i * top.ds);
         split_emit(p, sub, src_buf, fan_off, nfan, chunk_bytes);
+        if (p.too_many) return;
     }
 }
 
@@ -491,6 +526,7 @@ void emit_transpose(Plan &p, const TPiece &tp, int32_t src_buf, int64_t fan_off,
             sub.src_off = tp.src_off + uint64_t(i * top.ss);
             sub.dst_off = tp.dst_off + uint64_t(i * top.ds);
             emit_transpose(p, sub, src_buf, fan_off, nfan, chunk_bytes, out);
+            if (p.too_many || p.tile_span_too_long) return;
         }
         return;
     }
@@ -515,6 +551,7 @@ void emit_transpose(Plan &p, const TPiece &tp, int32_t src_buf, int64_t fan_off,
                     sub.src_off = tp.src_off + uint64_t(i * top.ss);
                     sub.dst_off = tp.dst_off + uint64_t(i * top.ds);
                     emit_transpose(p, sub, src_buf, fan_off, nfan, chunk_bytes, out);
+                    if (p.too_many || p.tile_span_too_long) return;
                 }
                 return;
             }
@@ -1094,6 +1131,7 @@ void lower(Plan &p) {
 
     std::vector<int64_t> ext_s(nd), ext_d(nd), str_s(nd), str_d(nd);
     for (size_t ti = 0; ti < p.tasks.size(); ++ti) {
+        if (p.too_many || p.tile_span_too_long) break;  // the plan fails: stop lowering
         if (handled[ti]) continue;
         const auto &t = p.tasks[ti];
         const int64_t fan_off = p.dst.shard_devs_off[t.dst_shard];
@@ -1193,6 +1231,7 @@ void lower(Plan &p) {
         }
         for (const auto &pc : parts) split_emit(p, pc, t.sender, fan_off, nfan, chunk);
     }
+    if (p.too_many || p.tile_span_too_long) return;  // the plan fails: nothing to order
     if (!(p.flags & 0x4u)) {
         // destination-major chunk order: receiver set, then the byte offset
         // of the chunk's first vector in the receivers' buffers

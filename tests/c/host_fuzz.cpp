@@ -4,7 +4,8 @@
 // extents 0..40, element sizes 1/2/4/8), meshes (1..3 axes of 1..4 devices)
 // and specs, under every lowering flag and several tunings; each plan runs
 // through the host interpreter on buffers of exactly the shard sizes, so any
-// access outside them is reported.  Prints "ok <plans>" on success.
+// access outside them is reported.  Then plans only, at sizes far beyond
+// this host's memory.  Prints "ok <plans>" on success.
 #include <cstdint>
 #include <cstdio>
 #include <cstdlib>
@@ -128,6 +129,65 @@ int main(int argc, char **argv) {
             for (auto q : dp) free(q);
             reshard_plan_destroy(p);
         }
+    }
+    // planning only, at sizes whose buffers would not fit this host: the two
+    // innermost extents up to 2^16, tensors of 2^32 to 2^35 bytes, permuted
+    // layouts included.
+    // Each plan either builds with read and written bytes equal to the
+    // definition (every element read once, every destination shard written
+    // once) or fails with a clean status and message.
+    for (int it = 0; it < iters / 10; ++it) {
+        const int nd = 2 + int(rnd(3));
+        const int di = int(rnd(4));
+        int64_t shape[4], numel = 1;
+        for (int d = 0; d < nd; ++d) {
+            shape[d] = d + 2 >= nd ? int64_t(1 + rnd(1u << 16)) : int64_t(1 + rnd(16));
+            numel *= shape[d];
+        }
+        if (numel * esz[di] < (int64_t(1) << 32) || numel * esz[di] > (int64_t(1) << 35)) {
+            --it;
+            continue;
+        }
+        const int smn = 1 + int(rnd(2)), dmn = 1 + int(rnd(2));
+        int64_t sm[2], dm[2];
+        for (int a = 0; a < smn; ++a) sm[a] = 1 + rnd(4);
+        for (int a = 0; a < dmn; ++a) dm[a] = 1 + rnd(4);
+        const std::string ss = random_spec(nd, smn), ds = random_spec(nd, dmn);
+        int32_t sperm[4], dperm[4];
+        for (int d = 0; d < nd; ++d) sperm[d] = dperm[d] = d;
+        for (int d = nd - 1; d > 0; --d) {
+            std::swap(sperm[d], sperm[rnd(uint32_t(d + 1))]);
+            std::swap(dperm[d], dperm[rnd(uint32_t(d + 1))]);
+        }
+        reshard_plan_t *p = nullptr;
+        const reshard_status_t st0 = reshard_plan_permuted(nd, shape, dts[di], smn, sm, ss.c_str(), sperm, dmn, dm,
+                                                           ds.c_str(), dperm, 0u, nullptr, &p);
+        if (st0 != RESHARD_OK) {
+            const char *e = reshard_last_error();
+            if (st0 != RESHARD_EUNSUPPORTED || !e || !*e) {
+                fprintf(stderr, "big plan: status %d: %s\n", int(st0), e ? e : "(null)");
+                return 1;
+            }
+            continue;
+        }
+        ++plans;
+        int64_t st[5];
+        reshard_plan_stats(p, &st[0], &st[1], &st[2], &st[3], &st[4]);
+        int64_t ndst = 1, written = 0;
+        for (int a = 0; a < dmn; ++a) ndst *= dm[a];
+        std::vector<int64_t> ls(nd);
+        for (int64_t k = 0; k < ndst; ++k) {
+            reshard_plan_local_shape(p, 1, k, ls.data());
+            int64_t n = esz[di];
+            for (int d = 0; d < nd; ++d) n *= ls[d];
+            written += n;
+        }
+        if (st[0] != numel * esz[di] || st[1] != written) {
+            fprintf(stderr, "big plan: bytes %lld/%lld, want %lld/%lld\n", (long long)st[0], (long long)st[1],
+                    (long long)(numel * esz[di]), (long long)written);
+            return 1;
+        }
+        reshard_plan_destroy(p);
     }
     for (int S = 1; S <= 6; ++S)
         for (int M = 1; M <= 9; M += 4) {

@@ -153,6 +153,19 @@ def test_tile_strides_beyond_31_bits_take_the_element_path():
     assert st["bytes_written"] == 200 * 34000000 and st["n_descriptors"] > 0
 
 
+def test_too_many_chunks_fails_cleanly():
+    # 29 GB of bytes whose source and destination orders share no run and
+    # whose strides keep them off the tile path: one chunk per few bytes,
+    # far beyond the descriptor budget -- refused, and lowering stops there
+    import time
+    t = time.time()
+    with pytest.raises(B.ReshardError) as e:
+        B.reshard_plan((16, 8, 5298, 42608), "uint8", (2,), "RS^{0}RR", (3,), "RRRR",
+                       src_perm=(0, 2, 3, 1), dst_perm=(2, 3, 1, 0))
+    assert e.value.status == B.RESHARD_EUNSUPPORTED and "2^24" in str(e.value)
+    assert time.time() - t < 60
+
+
 # --------------------------------------------------------------------- GPU
 
 def _gpu_run(shape, dt, sm, ss, sp, dm, ds, dp, seed=0, **kw):
