@@ -144,7 +144,9 @@ typedef struct {
  * together have more than RESHARD_MAX_BUFFERS devices, or the plan would need
  * more than 2^24 unit tasks or 2^24 workgroup chunks (automatic chunk sizes
  * grow with the tensor to stay well below; an explicit tuning.chunk_bytes can
- * exceed it); ENOMEM on allocation failure.  *out is set to NULL on error.
+ * exceed it, and so can a permuted layout whose rows lie so far apart that a
+ * chunk holds only a few of them -- lowering stops at the first chunk past
+ * the limit); ENOMEM on allocation failure.  *out is set to NULL on error.
  */
 reshard_status_t reshard_plan(int ndim, const int64_t *shape, reshard_dtype_t dtype,
                               int src_mesh_ndim, const int64_t *src_mesh, const char *src_spec,
