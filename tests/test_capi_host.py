@@ -443,6 +443,27 @@ def test_host_gather(case, chunk, band):
     host_case(shape, dt, sm, ss, dm, ds, flags=B.RESHARD_NO_GATHER)
 
 
+@pytest.mark.parametrize("shape", [(2, 64, 512), (4, 96, 768), (3, 50, 1024)])
+def test_gather_tail_halves_parity(shape):
+    # automatic chunk sizes cut the last fifth of the row-gather chunks in
+    # halves; the halves' origins come from the descriptor arithmetic,
+    # checked against the oracle through the host interpreter
+    args = (shape, "float16", (4, 8), "RRS^{01}", (4, 8), "RS^1R")
+    assert B.reshard_plan_gather_chunks(plan_of(*args)) > 0
+    host_case(*args)
+
+
+@pytest.mark.parametrize("wid", [3, 5])
+def test_gather_tail_halves_count(wid):
+    # at full size the automatic chunk is 16 KiB: the last fifth of the
+    # chunks become two each; an explicit chunk size keeps every chunk whole
+    w = WORKLOADS[wid]
+    args = (w.shape, w.dtype, w.src_mesh, w.src_spec, w.dst_mesh, w.dst_spec)
+    whole = B.reshard_plan_gather_chunks(plan_of(*args, chunk_bytes=16384))
+    assert whole == w.numel * w.itemsize // 16384
+    assert B.reshard_plan_gather_chunks(plan_of(*args)) == whole + whole // 5
+
+
 def test_gather_band_chunk_count():
     # bands tile the rows: same slots in total, each band's chunks separate
     shape, dt, sm, ss, dm, ds = GATHER_CASES[4]
