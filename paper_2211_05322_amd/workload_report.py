@@ -25,11 +25,19 @@ write), planning time, and four timings of `reshard_execute`:
 
 Each row ends with a round-trip check through the library (destination back
 to one buffer, compared bit for bit with the generated tensor).
+
+Each workload runs in a process of its own (as `bench.py` does), started by a
+parent that never touches the GPU: after other workloads' buffers have come
+and gone in the same process, the same launch measured up to 2 % slower on
+one machine (workload 5 rotated: 361.0 us alone, 366.2 us after workloads
+1-4).  `--one-process` keeps them in one process.
 """
 
 from __future__ import annotations
 
 import argparse
+import subprocess
+import sys
 import time
 
 import torch
@@ -150,6 +158,13 @@ def report_row(key, w, steps, flush_steps, scratch, stream):
     return row, ok
 
 
+def _print_header():
+    print("| id | workload | unit tasks | fan-out | chunks direct/gather/unaligned gather (slots/units)/transpose/realign | MB moved | "
+          "plan ms | "
+          "back-to-back µs | % | rotated µs (n) | % | cold µs | % | round trip | graph µs |")
+    print("|---" * 15 + "|", flush=True)  # (the chunks column lists six counts)
+
+
 def main():
     ap = argparse.ArgumentParser(description=__doc__.splitlines()[0])
     ap.add_argument("--steps", type=int, default=50)
@@ -157,23 +172,42 @@ def main():
     ap.add_argument("--flush-mib", type=int, default=1024)
     ap.add_argument("--workloads", default="1,2,3,4,5,uneven5,uneven3,uneven5_1rep,runs1,runs2,runs4,transposed2,transposed5,"
                                            "fanout1,fanout4,fanout8")
+    ap.add_argument("--one-process", action="store_true", help="run every workload in this process")
+    ap.add_argument("--rows-only", action="store_true", help=argparse.SUPPRESS)  # a child of the isolating parent
     a = ap.parse_args()
+    keys = a.workloads.split(",")
+    if not a.one_process and not a.rows_only:
+        # one child per workload; this process never initialises the GPU
+        print(f"One process per workload; back-to-back: mean of {a.steps} launches; rotated: the same over (n) "
+              f"buffer sets in turn; cold: mean of {a.flush_steps} launches, each after a read of {a.flush_mib} "
+              f"MiB; graph: per reshard, 50 captured executes replayed; % of {HBM_PEAK_GBS:.0f} GB/s\n")
+        _print_header()
+        failed = False
+        for key in keys:
+            r = subprocess.run([sys.executable, "-m", "paper_2211_05322_amd.workload_report", "--rows-only",
+                                "--steps", str(a.steps), "--flush-steps", str(a.flush_steps),
+                                "--flush-mib", str(a.flush_mib), "--workloads", key])
+            if r.returncode != 0:
+                failed = True
+                if r.returncode != 3:  # 3: a round-trip mismatch, reported in the row
+                    raise SystemExit(f"workload {key}: exit status {r.returncode}")
+        if failed:
+            raise SystemExit(3)
+        return
     if not torch.cuda.is_available():
         raise SystemExit("no GPU visible")
     B.load()
     torch.cuda.set_device(0)
     stream = torch.cuda.current_stream()
     scratch = torch.ones((a.flush_mib << 20) // 4, dtype=torch.int32, device="cuda")
-    print(f"{torch.cuda.get_device_name(0)}; back-to-back: mean of {a.steps} launches; rotated: the same "
-          f"over (n) buffer sets in turn; cold: mean of {a.flush_steps} launches, each after a read of "
-          f"{a.flush_mib} MiB; graph: per reshard, 50 captured executes replayed; % of "
-          f"{HBM_PEAK_GBS:.0f} GB/s\n")
-    print("| id | workload | unit tasks | fan-out | chunks direct/gather/unaligned gather (slots/units)/transpose/realign | MB moved | "
-          "plan ms | "
-          "back-to-back µs | % | rotated µs (n) | % | cold µs | % | round trip | graph µs |")
-    print("|---" * 15 + "|")  # (the chunks column lists six counts)
+    if not a.rows_only:
+        print(f"{torch.cuda.get_device_name(0)}; back-to-back: mean of {a.steps} launches; rotated: the same "
+              f"over (n) buffer sets in turn; cold: mean of {a.flush_steps} launches, each after a read of "
+              f"{a.flush_mib} MiB; graph: per reshard, 50 captured executes replayed; % of "
+              f"{HBM_PEAK_GBS:.0f} GB/s\n")
+        _print_header()
     all_ok = True
-    for key in a.workloads.split(","):
+    for key in keys:
         w = workload_by_name(key)
         row, ok = report_row(key, w, a.steps, a.flush_steps, scratch, stream)
         all_ok &= ok
