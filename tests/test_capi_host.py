@@ -453,6 +453,14 @@ def test_gather_tail_halves_parity(shape):
     host_case(*args)
 
 
+@pytest.mark.parametrize("band", [1, 3, 5])
+def test_gather_tail_halves_with_bands(band):
+    # column bands change the slot -> offset arithmetic the halves rely on
+    args = ((3, 64, 1024), "float16", (4, 8), "RRS^{01}", (4, 8), "RS^1R")
+    assert B.reshard_plan_gather_chunks(plan_of(*args, gather_band=band)) > 0
+    host_case(*args, gather_band=band)
+
+
 @pytest.mark.parametrize("wid", [3, 5])
 def test_gather_tail_halves_count(wid):
     # at full size the automatic chunk is 16 KiB: the last fifth of the
