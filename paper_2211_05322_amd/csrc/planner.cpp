@@ -598,10 +598,13 @@ void emit_transpose(Plan &p, const TPiece &tp, int32_t src_buf, int64_t fan_off,
     // most 256 tile rows (32 KiB of LDS); B extents wider than that take
     // 2 x 128 bytes, which keeps twice the tiles resident (measured: 512-byte
     // rows 382.6 us at 512-byte tiles against 391.6 at 256; 1 KiB rows 24.4
-    // against 26.2 us the other way)
+    // against 26.2 us the other way).  With one receiver, 2 x 128 bytes at
+    // most (measured: workload 5's tensor to one replica, 512-byte rows,
+    // 150.5 us against 152.6 at 512-byte tiles; with 4 replicas 512-byte
+    // tiles stay ahead, 381.2 against 388.3).
     uint32_t wide = 0;
     while (wide < RS_TMAXW_LOG2 && (te << wide) < tp.nb && (te << (wide + 1)) <= 256) ++wide;
-    if ((te << wide) < tp.nb && wide > 1) wide = 1;
+    if (((te << wide) < tp.nb || nfan == 1) && wide > 1) wide = 1;
     const int64_t tr = te << wide;
     const uint64_t ntb = uint64_t((tp.nb + tr - 1) / tr), nta = uint64_t((tp.na + te - 1) / te);
     const uint64_t tiles = ntb * nta * uint64_t(o1.n) * uint64_t(o2.n);
