@@ -251,7 +251,7 @@ reshard_status_t reshard_execute(const reshard_plan_t *plan, void *const *src_pt
  *
  * Errors: those of reshard_execute, and EUNSUPPORTED when the plan's tables
  * exceed RESHARD_NOALLOC_MAX_TABLE_BYTES (every workload of the paper's
- * shapes needs at most 2.7 MiB; larger chunks shrink the table).
+ * shapes needs at most 3.2 MiB; larger chunks shrink the table).
  */
 #define RESHARD_NOALLOC_MAX_TABLE_BYTES (4u << 20)
 reshard_status_t reshard_execute_noalloc(const reshard_plan_t *plan, void *const *src_ptrs,
