@@ -604,6 +604,16 @@ def test_fuzz_lowering_flags_and_tunings(case):
     assert_same(got, want)
 
 
+def test_fuzz_lowering_soak():
+    # 3,000 more cases of the generator above under a second seed, in one
+    # test (each printed before it runs)
+    for i, case in enumerate(_fuzz_lowering(3000, 90210)):
+        shape, dt, sm, ss, dm, ds, kw = case
+        _say(f"lowering soak {i} {case}")
+        got, want = run_gpu(shape, dt, sm, ss, dm, ds, rand_bits(shape, dt, zlib.crc32(repr(case).encode())), **kw)
+        assert_same(got, want)
+
+
 @pytest.mark.parametrize("dt", ["bfloat16", "int16", "int32", "int64"])
 def test_other_element_types(dt):
     """The kernels see only the element size: bf16 and the integer types go

@@ -227,6 +227,17 @@ def _tunings(n, seed):
 
 
 @pytest.mark.gpu
+def test_gpu_permuted_soak():
+    # 1,000 more permuted layouts under new seeds, each with its own chunk
+    # size and then a random launch tuning, in one test
+    for i, (case, tn) in enumerate(zip(perm_cases(1000, 5151, big=True), _tunings(1000, 5152))):
+        shape, dt, sm, ss, sp, dm, ds, dp, kw = case
+        for k in (kw, tn):
+            print(f"permuted soak {i} {case} {k}", flush=True)
+            _gpu_run(shape, dt, sm, ss, sp, dm, ds, dp, seed=i, **k)
+
+
+@pytest.mark.gpu
 @pytest.mark.parametrize("case,tuning", list(zip(perm_cases(120, 91), _tunings(120, 92))))
 def test_gpu_permuted_fuzz_tunings(case, tuning):
     # seeded permuted layouts under random chunk sizes, workgroup sizes and
