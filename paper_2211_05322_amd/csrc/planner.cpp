@@ -535,7 +535,7 @@ void emit_transpose(Plan &p, const TPiece &tp, int32_t src_buf, int64_t fan_off,
     {
         // every tile is addressed from the piece's origin: the piece must lie
         // within 32-bit offsets on both sides (else peel an outer level, or
-        // halve B in whole tiles)
+        // halve A or B in whole tiles)
         uint64_t ss_ = uint64_t(tp.nb - 1) * uint64_t(tp.ss_b) + uint64_t(tp.na * es);
         uint64_t sd_ = uint64_t(tp.na - 1) * uint64_t(tp.ds_a) + uint64_t(tp.nb * es);
         for (const auto &l : tp.outer) {
