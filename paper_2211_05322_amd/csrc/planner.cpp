@@ -1297,6 +1297,23 @@ void lower(Plan &p) {
     p.descs.insert(p.descs.begin() + std::ptrdiff_t(p.n_direct + p.n_gather), udescs.begin(), udescs.end());
     p.n_gather_u = udescs.size();
     p.n_unit = unitdescs.size();
+    if (!(p.flags & 0x4u)) {
+        // tile chunks in destination order too (receiver set, then the
+        // destination offset of the chunk's first tile), so the tiles
+        // resident together write neighbouring destination bytes whichever
+        // sender they read (same machine, interleaved: transposed workload 5
+        // 382.5 -> 372.3 us, fp32 385.6 -> 379.8, one replica 150.8 ->
+        // 147.4, source side permuted 409.5 -> 406.6; task order before)
+        std::vector<std::pair<std::pair<uint32_t, uint64_t>, size_t>> key(tdescs.size());
+        for (size_t i = 0; i < tdescs.size(); ++i) {
+            const Desc &d = tdescs[i];
+            key[i] = {{d.fan_off, d.dst_base + uint64_t(tile_offsets(d, d.v0, uint32_t(p.es)).dst)}, i};
+        }
+        std::stable_sort(key.begin(), key.end(), [](const auto &a, const auto &b) { return a.first < b.first; });
+        std::vector<Desc> sorted(tdescs.size());
+        for (size_t i = 0; i < key.size(); ++i) sorted[i] = tdescs[key[i].second];
+        tdescs.swap(sorted);
+    }
     p.descs.insert(p.descs.begin() + std::ptrdiff_t(p.n_direct + p.n_gather + p.n_gather_u), tdescs.begin(),
                    tdescs.end());
     p.n_transpose = tdescs.size();
